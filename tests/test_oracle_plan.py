@@ -1,0 +1,205 @@
+"""Pins for the plan oracle against what the paper and arithmetic fix (CPU only)."""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import plan as P
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rand_plan_inputs(rng, arch, L, H, dk):
+    shape = (L, H, dk) if arch == "kda" else (L, H)
+    a_log = rng.uniform(math.log(1e-4), 0.0, size=shape)
+    return P.static_log_decay(a_log)
+
+
+# ---- Eq. 2 / Eq. 3 -------------------------------------------------------------
+
+def test_softplus_identities():
+    # softplus(x) - softplus(-x) = x and softplus(0) = ln 2
+    for x in [-30.0, -2.5, -0.3, 0.0, 0.3, 1.7, 40.0]:
+        assert abs((P.softplus(x) - P.softplus(-x)) - x) <= 4e-16 * max(1.0, abs(x))
+    assert P.softplus(0.0) == math.log(2.0)
+    # against the textbook form ln(1 + e^x) where that form is accurate
+    for x in [-3.0, -0.3, 0.0, 0.7, 5.0]:
+        assert abs(P.softplus(x) - math.log(1.0 + math.exp(x))) <= 1e-15 * max(1.0, abs(x))
+
+
+def test_static_decay_closed_form():
+    # A_log = 0 and dt_bias = 0.3 cancel a = -0.3: g = -softplus(0) = -ln 2
+    g = P.static_log_decay(np.zeros(3), np.full(3, 0.3))
+    assert np.all(g == -math.log(2.0))
+    # g scales linearly in exp(A_log) = lambda and is always negative
+    lam = np.array([1e-4, 1e-2, 0.5, 1.0])
+    g = P.static_log_decay(np.log(lam))
+    sp = math.log1p(math.exp(-0.3))
+    np.testing.assert_allclose(g, -lam * sp, rtol=4e-15)  # exp(log(lam)) rounds
+    assert np.all(g < 0)
+
+
+def test_horizon_meaning():
+    # Eq. 3: after H_s tokens the decay factor e^{g H_s} equals eps
+    g = -np.array([1e-4, 3e-3, 0.05, 0.7, 5.0])
+    for eps in (1e-3, 1e-2):
+        Hs = P.horizon(g, eps)
+        np.testing.assert_allclose(np.exp(g * Hs), eps, rtol=1e-13)
+    # exact power-of-two case: g = ln(eps)/16 gives H_s = 16 exactly
+    g16 = math.log(1e-3) / 16.0
+    assert P.horizon(np.array([g16]))[0] == 16.0
+    with pytest.raises(ValueError):
+        P.horizon(np.array([0.0]))
+    with pytest.raises(ValueError):
+        P.horizon(np.array([0.1]))
+
+
+# ---- Sec. 4.1 selection ------------------------------------------------------------
+
+def test_dense_is_w_max_zero_and_large_w_keeps_nothing():
+    # App. C.1: dense is the same cache path with W_max = 0 (every unit retained)
+    rng = np.random.default_rng(1)
+    for arch in ("kda", "gdn"):
+        g = _rand_plan_inputs(rng, arch, 3, 4, 8)
+        p = P.build_plan(g, arch, 3, 4, 8, 8, w_max=0)
+        assert p["keep"].all() and p["n_rows"] == 3 * 4 * 8
+        np.testing.assert_array_equal(p["unit_row"], np.arange(3 * 4 * 8))
+        assert p["w_replay"] == 0
+        big = int(math.ceil(float(p["horizon"].max()))) + 1
+        p = P.build_plan(g, arch, 3, 4, 8, 8, w_max=big)
+        assert not p["keep"].any() and p["n_rows"] == 0
+        assert (p["inv_row"] == -1).all()
+
+
+def test_threshold_is_strict():
+    g16 = math.log(1e-3) / 16.0          # H_s = 16 exactly
+    g = np.array([[[g16, g16 * 0.5, g16 * 2.0]]])   # H_s = 16, 32, 8
+    p = P.build_plan(g, "kda", 1, 1, 3, 4, w_max=16)
+    np.testing.assert_array_equal(p["keep"][0, 0], [False, True, False])
+
+
+@pytest.mark.parametrize("arch", ["kda", "gdn"])
+def test_offsets_and_maps_against_brute_force(arch):
+    rng = np.random.default_rng(7)
+    L, H, dk, dv = 3, 4, 8, 4
+    for trial in range(6):
+        g = _rand_plan_inputs(rng, arch, L, H, dk)
+        w = int(rng.choice([0, 4, 16, 64, 256, 4096]))
+        p = P.build_plan(g, arch, L, H, dk, dv, w_max=w)
+        Hs = p["horizon"]
+        # independent route: a row is kept iff its unit's H_s > W_max; rows in dense order
+        row_keep = (Hs > w) if arch == "kda" else np.repeat((Hs > w)[..., None], dk, axis=-1)
+        row_keep = row_keep.reshape(-1)
+        np.testing.assert_array_equal(p["unit_row"], np.flatnonzero(row_keep))
+        assert p["n_rows"] == row_keep.sum() == p["off"][-1]
+        inv = p["inv_row"]
+        np.testing.assert_array_equal(inv[p["unit_row"]], np.arange(p["n_rows"]))
+        assert (inv >= 0).sum() == p["n_rows"]
+        per_lh = row_keep.reshape(L * H, dk).sum(axis=1)
+        np.testing.assert_array_equal(np.diff(p["off"]), per_lh)
+        # App. B: o_0 = 0, o_{l+1} = o_l + r_l (units)
+        r_l = (Hs > w).reshape(L, -1).sum(axis=1)
+        np.testing.assert_array_equal(p["layer_off"], np.concatenate([[0], np.cumsum(r_l)]))
+
+
+def test_topk_modes_brute_force_with_ties():
+    H = np.array([[[5.0, 9.0, 9.0, 1.0, 9.0, 2.0],
+                   [3.0, 3.0, 3.0, 3.0, 3.0, 3.0]]])
+    keep = P.select(H, "kda", "topk_head", w_max=0, keep_k=2)
+    np.testing.assert_array_equal(keep[0, 0], [False, True, True, False, False, False])
+    np.testing.assert_array_equal(keep[0, 1], [True, True, False, False, False, False])
+    keep = P.select(H, "kda", "topk_layer", w_max=0, keep_k=5)
+    # layer ranking: 9,9,9 (idx 1,2,4), then 5 (idx 0), then ties at 3 -> lowest idx 6
+    want = np.zeros(12, dtype=bool)
+    want[[1, 2, 4, 0, 6]] = True
+    np.testing.assert_array_equal(keep.reshape(-1), want)
+    rng = np.random.default_rng(3)
+    for _ in range(20):
+        Hs = np.round(rng.uniform(1, 10, size=(2, 3, 5)), 0)      # many ties
+        k = int(rng.integers(0, 16))
+        keep = P.select(Hs, "kda", "topk_layer", w_max=0, keep_k=k)
+        for l in range(2):
+            flat, kf = Hs[l].reshape(-1), keep[l].reshape(-1)
+            assert kf.sum() == k
+            for i in np.flatnonzero(kf):
+                for j in np.flatnonzero(~kf):
+                    assert flat[i] > flat[j] or (flat[i] == flat[j] and i < j)
+
+
+# ---- Eq. 7 ----------------------------------------------------------------------
+
+def test_replay_window_golden():
+    cases = json.load(open(os.path.join(GOLD, "replay_window.json")))["cases"]
+    for c in cases:
+        assert P.replay_window(c["h"], c["w_max"]) == c["w"], c
+
+
+def test_w_replay_is_max_over_omitted_only():
+    g16 = math.log(1e-3) / 16.0
+    # H_s = 16 (omitted at W_max=64 -> W 16), 5.3-ish, and 200 (kept -> ignored)
+    g = np.array([[g16, math.log(1e-3) / 5.3, math.log(1e-3) / 200.0]])
+    p = P.build_plan(g, "gdn", 1, 3, 4, 4, w_max=64)
+    np.testing.assert_array_equal(p["keep"][0], [False, False, True])
+    assert p["w_replay"] == 16
+    np.testing.assert_array_equal(p["w_units"][0], [16, 8, 0])
+
+
+# ---- Sec. 4.3 rank slices ----------------------------------------------------------
+
+@pytest.mark.parametrize("arch,T", [("kda", 1), ("kda", 4), ("kda", 8), ("gdn", 4)])
+def test_rank_slices_and_send_matrix(arch, T):
+    rng = np.random.default_rng(11 + T)
+    L, H, dk = 3, 8, 8
+    g = _rand_plan_inputs(rng, arch, L, H, dk)
+    p = P.build_plan(g, arch, L, H, dk, 4, w_max=16, n_ranks=T)
+    R_units = p["n_units"]
+    C = p["slice_units"]
+    assert C == -(-R_units // T)
+    rb = p["rank_begin"] // p["rows_per_unit"]
+    assert rb[0] == 0 and rb[-1] == R_units and np.all(np.diff(rb) <= C)
+    send = p["send"]
+    assert send.sum() == R_units
+    # row sums: units whose head is computed on rank o (brute force)
+    owned = np.zeros(T, dtype=np.int64)
+    for l in range(L):
+        for h in range(H):
+            owned[h // (H // T)] += int(p["unit_count"][l, h])
+    np.testing.assert_array_equal(send.sum(axis=1), owned)
+    np.testing.assert_array_equal(send.sum(axis=0), np.diff(rb))
+
+
+# ---- Eq. 6 / App. B ratios -----------------------------------------------------------
+
+def test_compression_ratios_closed_form():
+    # L = 2 layers of n_l = 4 units (GDN heads); keep 1 and 3 heads
+    g_keep, g_omit = math.log(1e-3) / 1000.0, math.log(1e-3) / 2.0
+    g = np.array([[g_keep, g_omit, g_omit, g_omit], [g_keep, g_keep, g_keep, g_omit]])
+    p = P.build_plan(g, "gdn", 2, 4, 2, 2, w_max=16, conv_bytes=10)
+    assert p["c_temp_rag"] == 8 / 4
+    assert p["c_temp_pad"] == 8 / (2 * 3)
+    assert p["layout_gain"] == 3 / 2
+    assert math.isclose(p["c_temp_rag"] / p["c_temp_pad"], p["layout_gain"], rel_tol=1e-15)
+    ub = 2 * 2 * 4
+    assert p["c_ckpt"] == (8 * ub + 10) / (4 * ub + 10)
+
+
+def test_matched_hbm_slots_golden():
+    gold = json.load(open(os.path.join(GOLD, "matched_hbm.json")))
+    for arch in ("kda", "gdn"):
+        b = gold[arch]["budget_bytes"]
+        per_slot = b // gold[arch]["dense_physical_slots"]
+        assert per_slot * gold[arch]["dense_physical_slots"] == b
+        assert P.matched_slots(b, per_slot) == gold[arch]["deployable_slots"]
+        # the same budget through a dense plan (W_max = 0) at the model's per-rank shape
+        s = gold["derived_shapes"][arch]
+        shape = (s["n_layers"], s["n_heads"], s["dk"]) if arch == "kda" else (s["n_layers"], s["n_heads"])
+        g = np.full(shape, -0.1)
+        p = P.build_plan(g, arch, s["n_layers"], s["n_heads"], s["dk"], s["dv"], w_max=0,
+                         n_ranks=s["tp"], conv_bytes=s["conv_bytes_per_rank"])
+        assert p["dense_slot_bytes_rank"] == per_slot
+        assert p["slot_bytes_rank"] == per_slot
+        assert P.matched_slots(b, p["slot_bytes_rank"]) == 127
+        assert p["c_ckpt"] == 1.0
