@@ -1,0 +1,230 @@
+/*
+ * dasc.h -- C ABI of the DASC state-checkpoint library for MI355X (gfx950).
+ *
+ * DASC ("Decay-Aware State Compression for Hybrid Linear-Attention Serving")
+ * keeps only the long-horizon units of a gated delta-rule recurrent state in a
+ * prefix-cache checkpoint, and on reuse either leaves the omitted units at zero
+ * or refreshes them by replaying a bounded suffix.  This library implements
+ * that path for one GPU:
+ *
+ *   dasc_plan     static selection plan from weight-derived decay (host only)
+ *   dasc_pack     Store: ragged gather of retained units into checkpoint slots
+ *   dasc_restore  Load:  scatter retained units back, omitted units = +0.0
+ *   dasc_refresh  Load with refresh: replay the last W tokens of the gated
+ *                 delta rule and overwrite only the omitted units
+ *
+ * State layout.  The paper writes a head state as S in R^{dv x dk} (Sec. 3.1,
+ * Eq. 1).  This library stores its transpose S' = S^T as [dk, dv] fp32, dv
+ * contiguous, so one KDA unit -- the key channel (h, k) of Sec. 4.1 -- is one
+ * contiguous row of dv floats, and one GDN unit (a whole head) is dk such rows.
+ * An active-state pool is [n_pool, L, H, dk, dv] fp32; a checkpoint pool is
+ * [T, n_slots, C_rows, dv] fp32 (T = 1, C_rows = R for the flat layout).
+ *
+ * Conventions for every call.
+ *   - Returns DASC_OK (0) or a negative DASC_E_* code; nothing throws or aborts.
+ *   - Every argument the host can see is validated before any launch; a failed
+ *     check returns an error and launches nothing.
+ *   - The caller owns all memory.  The library allocates no device memory and
+ *     keeps no state between calls.
+ *   - Device calls are asynchronous on the given stream and never synchronise.
+ *     A NULL stream means the default (null) stream.
+ *   - Indices that live in device memory (slot lists, row maps) cannot be seen
+ *     by the host.  Kernels check each against its bound: a checkpoint whose
+ *     slot index is out of range is skipped (nothing written for it), a packed
+ *     row whose dense row is out of range is not written, and restore treats a
+ *     dense row whose packed index is out of range as omitted (+0.0).
+ *   - Device pointers to fp32 state/checkpoint data must be 16-byte aligned and
+ *     dv must be a multiple of 4 (each row moves as 128-bit words).
+ */
+#ifndef DASC_H
+#define DASC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------- */
+#define DASC_OK             0
+#define DASC_E_INVAL       -1  /* null pointer, misalignment, scalar out of range */
+#define DASC_E_SHAPE       -2  /* shape fields inconsistent with each other      */
+#define DASC_E_WORKSPACE   -3  /* workspace smaller than dasc_refresh_workspace_bytes */
+#define DASC_E_HIP         -4  /* the HIP runtime reported an error at launch    */
+#define DASC_E_UNSUPPORTED -5  /* valid request with no kernel built for it      */
+
+/* ---- enumerations -------------------------------------------------------- */
+#define DASC_ARCH_KDA 0  /* channel-wise decay: unit = one (head, key channel) row */
+#define DASC_ARCH_GDN 1  /* head-wise decay:    unit = one whole head              */
+
+#define DASC_KEEP_THRESHOLD      0  /* keep u iff H_s(u) > W_max (Sec. 4.1)           */
+#define DASC_KEEP_TOPK_PER_HEAD  1  /* keep the keep_k longest-horizon channels per head (KDA) */
+#define DASC_KEEP_TOPK_PER_LAYER 2  /* keep the keep_k longest-horizon units per layer */
+
+#define DASC_INIT_RESTORED 0  /* refresh replays from the restored active state      */
+#define DASC_INIT_ZERO     1  /* refresh replays from a zero scratch state (Sec. 4.2) */
+
+/* hipStream_t is `struct ihipStream_t *`; declared here so callers need no HIP headers. */
+struct ihipStream_t;
+typedef struct ihipStream_t *dasc_stream_t;
+
+/* Shape of one recurrent state (all layers of one checkpoint). */
+typedef struct dasc_shape {
+  int32_t arch;        /* DASC_ARCH_KDA or DASC_ARCH_GDN                          */
+  int32_t n_layers;    /* L: recurrent (linear-attention) layers                 */
+  int32_t n_heads;     /* H: state (value) heads per layer                       */
+  int32_t n_qk_heads;  /* Hqk: key heads per layer; value head j reads key head
+                          j / (H / Hqk).  H % Hqk == 0.                          */
+  int32_t dk;          /* key dimension: rows of a head state                    */
+  int32_t dv;          /* value dimension: fp32 words per row, multiple of 4     */
+} dasc_shape;
+
+/* ---- plan (host only) ---------------------------------------------------- */
+
+/* Static log-decay of Sec. 3.3, Eq. 2: g[i] = -exp(a_log[i]) * softplus(a + dt_bias[i]),
+ * with softplus(x) = max(x, 0) + log1p(exp(-|x|)) in binary64.  The paper fixes the
+ * input-dependent logit at a = -0.3.  dt_bias may be NULL (taken as 0).  Host arrays of
+ * n doubles; g_out is written.  Errors: DASC_E_INVAL for NULL a_log/g_out or n < 0. */
+int dasc_static_log_decay(const double *a_log, const double *dt_bias, double a, int64_t n,
+                          double *g_out);
+
+typedef struct dasc_plan_desc {
+  dasc_shape shape;
+  int32_t keep_mode;   /* DASC_KEEP_*                                             */
+  int32_t keep_k;      /* units kept per head / per layer in the top-k modes      */
+  int32_t w_max;       /* W_max (tokens), >= 0: threshold of Sec. 4.1 and upper
+                          clamp of Eq. 7.  W_max = 0 keeps every unit ("dense").  */
+  int32_t n_ranks;     /* T >= 1: TP degree for the per-rank slice table          */
+  double eps;          /* epsilon of Eq. 3, in (0, 1); the paper uses 1e-3        */
+  int64_t conv_bytes;  /* per-rank conv-state bytes per slot (Eq. 6 C_ckpt), >= 0 */
+} dasc_plan_desc;
+
+/* Plan outputs.  Array members are caller-owned HOST buffers whose sizes follow
+ * from the shape alone (n_units_total = L*H*dk for KDA, L*H for GDN); a NULL
+ * member is skipped.  Scalars are always written. */
+typedef struct dasc_plan_out {
+  uint8_t *keep;          /* [n_units_total] 1 = retained (global), 0 = omitted (local) */
+  double *horizon;        /* [n_units_total] H_s = ln(eps) / g (Eq. 3)                  */
+  int32_t *unit_count;    /* [L*H] retained units of each (layer, head)                 */
+  int32_t *off;           /* [L*H+1] first packed row of each (layer, head); off[L*H] = R */
+  int32_t *layer_off;     /* [L+1] App. B offsets o_l in units: o_0 = 0, o_{l+1} = o_l + r_l */
+  int32_t *unit_row;      /* [L*H*dk] capacity: dense row (l*H + h)*dk + c of packed row j,
+                             j < R, in (layer, head, channel) order                     */
+  int32_t *inv_row;       /* [L*H*dk] packed row of each dense row, -1 if omitted       */
+  int32_t *w_units;       /* [n_units_total] Eq. 7 window of each omitted unit, 0 if kept */
+  int32_t *rank_begin;    /* [T+1] first packed row of each rank slice; rank_begin[T] = R */
+  int64_t *send;          /* [T*T] send[o*T + s]: units computed on rank o (owner
+                             floor(h*T/H)) that are stored in rank s's slice (Sec. 4.3) */
+  int64_t n_rows;         /* R: packed rows per checkpoint                              */
+  int64_t n_units;        /* retained units, sum_l r_l                                  */
+  int32_t rows_per_unit;  /* 1 (KDA) or dk (GDN)                                        */
+  int32_t w_replay;       /* Eq. 7: max window over omitted units, 0 if none            */
+  int64_t slice_units;    /* C = ceil(n_units / T) (Sec. 4.3)                           */
+  int64_t slice_rows;     /* C * rows_per_unit: rows of one rank slice                  */
+  double c_temp_rag;      /* Eq. 6: sum_l n_l / sum_l r_l (inf if nothing retained)    */
+  double c_temp_pad;      /* Sec. 4.1 padded layout: sum_l n_l / (L * R_max)            */
+  double layout_gain;     /* R_max / r_bar (App. B)                                     */
+  double c_ckpt;          /* Eq. 6 C_ckpt with per-rank bottleneck: (dense/T + conv) /
+                             (C * unit bytes + conv)                                    */
+  int64_t slot_bytes_rank;       /* C * unit bytes + conv_bytes (Eq. 8 b_bottleneck)    */
+  int64_t dense_slot_bytes_rank; /* ceil(n_units_total / T) * unit bytes + conv_bytes   */
+} dasc_plan_out;
+
+/* Build the static plan (Sec. 3.3, Sec. 4.1-4.3, App. B) from per-unit static
+ * log-decay g_static (host, [L,H,dk] for KDA or [L,H] for GDN, every entry finite
+ * and < 0).  Selection: DASC_KEEP_THRESHOLD keeps u iff H_s(u) > w_max (equality
+ * omits); the top-k modes rank by H_s descending with ties to the lower unit index.
+ * Pure host function: deterministic, bit-identical for identical inputs, no device use.
+ * Errors: DASC_E_INVAL (NULL desc/g_static/out, eps not in (0,1), g not finite and
+ * negative, w_max < 0, n_ranks < 1, keep_k out of range, conv_bytes < 0),
+ * DASC_E_SHAPE (non-positive dims, H % Hqk != 0, per-head top-k on GDN,
+ * L*H*dk >= 2^31). */
+int dasc_plan(const dasc_plan_desc *desc, const double *g_static, dasc_plan_out *out);
+
+/* App. C.1, Eq. 8: *slots = floor(budget_bytes / slot_bytes) - 1 (allocator slot 0 is
+ * reserved).  Errors: DASC_E_INVAL if slots is NULL, budget_bytes < 0 or slot_bytes <= 0. */
+int dasc_matched_slots(int64_t budget_bytes, int64_t slot_bytes, int64_t *slots);
+
+/* Static message for a status code (never NULL). */
+const char *dasc_strerror(int code);
+
+/* ---- Store: ragged pack (Sec. 4.1, App. B "Scheme 2") -------------------- */
+
+/* For i < n and packed row j < n_rows:
+ *     ckpt[r][dst_slot[i]][j - r*slice_rows][:] = states[src_slot[i]][unit_row[j]][:],
+ *     r = j / slice_rows,
+ * a bit-exact copy of dv fp32 words.  States are a pool [n_pool, L, H, dk, dv] whose
+ * rows are addressed as [n_pool, L*H*dk, dv]; ckpt is [n_ranks, n_ckpt_slots,
+ * slice_rows, dv].  n_ranks = 1 with slice_rows = n_rows is the flat layout
+ * [n_ckpt_slots, R, dv]; n_ranks = T with slice_rows = the plan's slice_rows is the
+ * per-rank slice layout of Sec. 4.3 (one device).  Checkpoint rows no packed row maps
+ * to are not written.
+ *   states, ckpt: device, 16-byte aligned.  src_slot, dst_slot: device int32 [n].
+ *   unit_row: device int32 [n_rows] (dasc_plan's unit_row).
+ * Errors: DASC_E_INVAL (NULL pointer with n > 0 and n_rows > 0, misalignment, n < 0,
+ * n_pool < 1, n_ckpt_slots < 1, n_ranks < 1, slice_rows * n_ranks < n_rows),
+ * DASC_E_SHAPE (bad shape, n_rows > L*H*dk, dv % 4 != 0), DASC_E_HIP. */
+int dasc_pack(const dasc_shape *shape,
+              const float *states, int64_t n_pool, const int32_t *src_slot,
+              const int32_t *unit_row, int64_t n_rows,
+              float *ckpt, int64_t n_ckpt_slots, const int32_t *dst_slot,
+              int32_t n_ranks, int64_t slice_rows, int32_t n, dasc_stream_t stream);
+
+/* ---- Load without refresh: restore with zero-fill (Sec. 4.2, DASC-NR) ----- */
+
+/* For i < n and every dense row d < L*H*dk of the destination state:
+ *     p = inv_row[d];
+ *     states[dst_slot[i]][d][:] = (0 <= p < n_rows) ? ckpt[r][src_slot[i]][p - r*slice_rows][:]
+ *                                                   : +0.0 (all bits clear),
+ *     r = p / slice_rows.
+ * Every row of every destination state is written (no separate memset needed).
+ *   ckpt, states: device, 16-byte aligned.  inv_row: device int32 [L*H*dk]
+ *   (dasc_plan's inv_row).  src_slot, dst_slot: device int32 [n].
+ * Errors: as dasc_pack. */
+int dasc_restore(const dasc_shape *shape,
+                 const float *ckpt, int64_t n_ckpt_slots, const int32_t *src_slot,
+                 int32_t n_ranks, int64_t slice_rows, int64_t n_rows,
+                 const int32_t *inv_row,
+                 float *states, int64_t n_pool, const int32_t *dst_slot,
+                 int32_t n, dasc_stream_t stream);
+
+/* ---- Load with refresh: bounded-suffix replay (Sec. 4.2 DASC-WR, Eq. 1) --- */
+
+/* Device workspace dasc_refresh needs for n_req requests and window W (may be 0).
+ * Errors: DASC_E_INVAL (NULL shape/bytes, n_req < 1, W < 1), DASC_E_SHAPE. */
+int dasc_refresh_workspace_bytes(const dasc_shape *shape, int32_t n_req, int32_t W,
+                                 size_t *bytes);
+
+/* Replay the gated delta rule of Eq. 1 over the last W tokens for one layer and
+ * overwrite only the omitted units, for each request i < n_req whose active state is
+ * pool slot slot[i].  With S' = S^T (rows = key channels), per token t:
+ *     S~  = Diag(exp(g_t)) S'_{t-1}
+ *     S'_t = S~ + beta_t k_t (v_t - S~^T k_t)^T
+ * S'_0 is the head's current (restored) state (DASC_INIT_RESTORED) or zero
+ * (DASC_INIT_ZERO).  KDA: rows c with inv_row[(layer*H + h)*dk + c] < 0 receive
+ * S'_W[c]; all other rows keep their bits.  GDN: a head is omitted when its rows are,
+ * and its whole state receives S'_W.  Heads with nothing omitted are not touched.
+ *   inv_row: device int32 [L*H*dk] (dasc_plan's inv_row; only the sign is read).
+ *   states:  device fp32 pool [n_pool, L, H, dk, dv], 16-byte aligned, read and written.
+ *   slot:    device int32 [n_req].
+ *   k:    device bf16 bits [n_req, Hqk, W, dk]   (16-byte aligned, dk % 8 == 0)
+ *   v:    device bf16 bits [n_req, H,   W, dv]   (16-byte aligned)
+ *   g:    device fp32 log-gates, [n_req, H, W, dk] (KDA) or [n_req, H, W] (GDN)
+ *   beta: device fp32 [n_req, H, W]
+ *   workspace: device, at least dasc_refresh_workspace_bytes (may be NULL if that is 0).
+ * Arithmetic is fp32 with bf16 inputs widened exactly.
+ * Errors: DASC_E_INVAL (NULL pointer, misalignment, layer out of [0, L), n_req < 1,
+ * W < 1, bad init_mode, n_pool < 1), DASC_E_SHAPE (bad shape), DASC_E_WORKSPACE,
+ * DASC_E_UNSUPPORTED (dk not in {16, 32, 64, 128} or dv > 256), DASC_E_HIP. */
+int dasc_refresh(const dasc_shape *shape, int32_t layer, const int32_t *inv_row,
+                 float *states, int64_t n_pool, const int32_t *slot,
+                 const uint16_t *k, const uint16_t *v, const float *g, const float *beta,
+                 int32_t n_req, int32_t W, int32_t init_mode,
+                 void *workspace, size_t workspace_bytes, dasc_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DASC_H */

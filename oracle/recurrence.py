@@ -117,7 +117,7 @@ def replay_chunked(S0: np.ndarray, k: np.ndarray, v: np.ndarray, g: np.ndarray, 
 
 def refresh(states: np.ndarray, inv_row_layer: np.ndarray, k_bits: np.ndarray, v_bits: np.ndarray,
             g: np.ndarray, beta: np.ndarray, n_qk_heads: int, init: str = "restored",
-            heads: list | None = None, requests: list | None = None):
+            pairs: list | None = None):
     """Sec. 4.2 refresh of one layer.
 
     states        [n_req, H, dk, dv] fp32: the restored active states (input)
@@ -126,41 +126,44 @@ def refresh(states: np.ndarray, inv_row_layer: np.ndarray, k_bits: np.ndarray, v
     g             [n_req, H, W, dk] (KDA) or [n_req, H, W] (GDN) fp32; beta [n_req, H, W] fp32
     init          "restored" (start from the restored state) or "zero" (the paper's
                   zero-initialised scratch state)
-    heads/requests  optional subsets to evaluate (others are returned unchanged)
+    pairs         optional list of (request, head) to evaluate; default all of them
 
-    Returns (out, omitted): out float64 [n_req, H, dk, dv] where omitted rows hold the
+    Returns (out, omitted): out float64 [len(pairs), dk, dv] where omitted rows hold the
     replayed state and every other row the input value; omitted [H, dk] bool.
-    A head is replayed as a whole because its rows are coupled through S~^T k_t.
+    A head is replayed as a whole because its rows are coupled through S~^T k_t;
+    a head with nothing omitted is returned unchanged.
     """
     n_req, H, dk, dv = states.shape
     omitted = (np.asarray(inv_row_layer).reshape(H, dk) < 0)
-    out = np.asarray(states, dtype=np.float64).copy()
     group = H // n_qk_heads
-    heads = range(H) if heads is None else heads
-    requests = range(n_req) if requests is None else requests
-    for h in heads:
-        if not omitted[h].any():
-            continue
-        hk = h // group
-        for n in requests:
-            S0 = out[n, h] if init == "restored" else np.zeros((dk, dv))
-            SW = replay_naive(S0, widen_bf16(k_bits[n, hk]), widen_bf16(v_bits[n, h]),
-                              g[n, h], beta[n, h])
-            out[n, h][omitted[h]] = SW[omitted[h]]
+    if pairs is None:
+        pairs = [(n, h) for n in range(n_req) for h in range(H)]
+    out = np.stack([np.asarray(states[n, h], dtype=np.float64) for n, h in pairs])
+    todo = [i for i, (n, h) in enumerate(pairs) if omitted[h].any()]
+    if todo:
+        S0 = out[todo] if init == "restored" else np.zeros((len(todo), dk, dv))
+        k = np.stack([widen_bf16(k_bits[pairs[i][0], pairs[i][1] // group]) for i in todo])
+        v = np.stack([widen_bf16(v_bits[pairs[i]]) for i in todo])
+        gg = np.stack([g[pairs[i]] for i in todo])
+        bb = np.stack([beta[pairs[i]] for i in todo])
+        SW = replay_naive(S0, k, v, gg, bb)
+        for b, i in enumerate(todo):
+            m = omitted[pairs[i][1]]
+            out[i][m] = SW[b][m]
     return out, omitted
 
 
-def refresh_error(got: np.ndarray, want: np.ndarray, omitted: np.ndarray) -> float:
+def refresh_error(got: np.ndarray, want: np.ndarray, omitted: np.ndarray, pairs: list) -> float:
     """Largest per-(request, head) error over refreshed rows, normalised by that head's
-    largest refreshed magnitude: max |got - want| / max |want|."""
+    largest refreshed magnitude: max |got - want| / max |want|.
+
+    got, want: [len(pairs), dk, dv]; omitted: [H, dk]."""
     worst = 0.0
-    n_req, H = want.shape[:2]
-    for n in range(n_req):
-        for h in range(H):
-            m = omitted[h]
-            if not m.any():
-                continue
-            ref = np.abs(want[n, h][m]).max()
-            err = np.abs(np.asarray(got[n, h], dtype=np.float64)[m] - want[n, h][m]).max()
-            worst = max(worst, err / ref if ref > 0 else err)
+    for i, (_, h) in enumerate(pairs):
+        m = omitted[h]
+        if not m.any():
+            continue
+        ref = np.abs(want[i][m]).max()
+        err = np.abs(np.asarray(got[i], dtype=np.float64)[m] - want[i][m]).max()
+        worst = max(worst, err / ref if ref > 0 else err)
     return worst

@@ -1,0 +1,218 @@
+// Ragged pack (Store) and zero-fill restore (Load) of DASC state checkpoints.
+//
+// Sec. 4.1 / App. B "Scheme 2": the retained units of all layers are flat-packed,
+// layer after layer, into one checkpoint of sum_l r_l units.  Sec. 4.2: on a hit the
+// retained units are loaded exactly and the omitted units stay at zero.  Sec. 4.3:
+// with T ranks the packed units are cut into slices of C units (one device here).
+//
+// Both kernels are HBM-bound bit copies.  A state row (one KDA unit, or one of the
+// dk rows of a GDN unit) is dv fp32 words = dv/4 128-bit vectors, 512 B at dv = 128.
+// A 256-thread block owns a tile of rows of one checkpoint; each thread issues
+// UNROLL independent 128-bit loads before its stores so that enough reads are in
+// flight per CU to cover HBM latency.  The per-row index (unit_row / inv_row) is a
+// single 32-bit load shared by the dv/4 lanes of that row.  Destination stores are
+// non-temporal: nothing reads a freshly written checkpoint or state back from cache.
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "dasc.h"
+#include "launch_common.h"
+
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;
+constexpr int kVecPerBlock = kThreads * kUnroll;  // 128-bit vectors moved per block
+
+// VPR_LOG2 >= 0: dv/4 is the power of two 2^VPR_LOG2 (shift/mask addressing).
+// VPR_LOG2 <  0: dv/4 given at run time (division addressing).
+template <int VPR_LOG2>
+struct RowGeom {
+  __device__ static int vpr(int) { return 1 << VPR_LOG2; }
+  __device__ static int row_of(int v, int) { return v >> VPR_LOG2; }
+  __device__ static int col_of(int v, int) { return v & ((1 << VPR_LOG2) - 1); }
+};
+template <>
+struct RowGeom<-1> {
+  __device__ static int vpr(int rt) { return rt; }
+  __device__ static int row_of(int v, int rt) { return v / rt; }
+  __device__ static int col_of(int v, int rt) { return v % rt; }
+};
+
+// Row offset (in rows) of packed row j of checkpoint slot `slot` in the
+// [T, n_slots, slice_rows] layout; the flat layout (one slice) needs no division.
+__device__ inline int64_t slice_row(int64_t j, int64_t slice_rows, int64_t n_rows,
+                                    int64_t n_slots, int64_t slot) {
+  const int64_t r = slice_rows >= n_rows ? 0 : int64_t(uint32_t(j) / uint32_t(slice_rows));
+  return (r * n_slots + slot) * slice_rows + (j - r * slice_rows);
+}
+
+// Rows per block: enough 128-bit vectors for every thread to move kUnroll of them.
+inline int rows_per_block(int vpr) { return vpr >= kVecPerBlock ? 1 : kVecPerBlock / vpr; }
+
+template <int VPR_LOG2>
+__global__ __launch_bounds__(kThreads) void pack_kernel(
+    const f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
+    const int32_t* __restrict__ src_slot, const int32_t* __restrict__ unit_row, int64_t n_rows,
+    f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ dst_slot,
+    int64_t slice_rows, int blocks_per_ckpt, int rpb, int vpr_rt) {
+  using G = RowGeom<VPR_LOG2>;
+  const int vpr = G::vpr(vpr_rt);
+  const int i = blockIdx.x / blocks_per_ckpt;
+  const int rb = blockIdx.x - i * blocks_per_ckpt;
+  const int64_t s = src_slot[i];
+  const int64_t d = dst_slot[i];
+  if (s < 0 || s >= n_pool || d < 0 || d >= n_ckpt_slots) return;
+  const f32x4* src = states + s * rows_state * vpr;
+  const int64_t row0 = int64_t(rb) * rpb;
+  const int n_vec = rpb * vpr;
+
+  for (int base = 0; base < n_vec; base += kVecPerBlock) {
+    f32x4 val[kUnroll];
+    int64_t dst_off[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int v = base + u * kThreads + threadIdx.x;
+      const int64_t j = row0 + G::row_of(v, vpr_rt);
+      dst_off[u] = -1;
+      if (v < n_vec && j < n_rows) {
+        const int64_t dense = unit_row[j];
+        if (dense >= 0 && dense < rows_state) {
+          const int c = G::col_of(v, vpr_rt);
+          val[u] = __builtin_nontemporal_load(src + dense * vpr + c);
+          dst_off[u] = slice_row(j, slice_rows, n_rows, n_ckpt_slots, d) * vpr + c;
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+      if (dst_off[u] >= 0) __builtin_nontemporal_store(val[u], ckpt + dst_off[u]);
+  }
+}
+
+template <int VPR_LOG2>
+__global__ __launch_bounds__(kThreads) void restore_kernel(
+    const f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ src_slot,
+    int64_t slice_rows, int64_t n_rows, const int32_t* __restrict__ inv_row,
+    f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
+    const int32_t* __restrict__ dst_slot, int blocks_per_state, int rpb, int vpr_rt) {
+  using G = RowGeom<VPR_LOG2>;
+  const int vpr = G::vpr(vpr_rt);
+  const int i = blockIdx.x / blocks_per_state;
+  const int rb = blockIdx.x - i * blocks_per_state;
+  const int64_t s = src_slot[i];
+  const int64_t d = dst_slot[i];
+  if (s < 0 || s >= n_ckpt_slots || d < 0 || d >= n_pool) return;
+  f32x4* dst = states + d * rows_state * vpr;
+  const int64_t row0 = int64_t(rb) * rpb;
+  const int n_vec = rpb * vpr;
+
+  for (int base = 0; base < n_vec; base += kVecPerBlock) {
+    f32x4 val[kUnroll];
+    int64_t dst_off[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int v = base + u * kThreads + threadIdx.x;
+      const int64_t dense = row0 + G::row_of(v, vpr_rt);
+      dst_off[u] = -1;
+      val[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (v < n_vec && dense < rows_state) {
+        const int c = G::col_of(v, vpr_rt);
+        const int64_t p = inv_row[dense];
+        if (p >= 0 && p < n_rows) {
+          val[u] = __builtin_nontemporal_load(
+              ckpt + slice_row(p, slice_rows, n_rows, n_ckpt_slots, s) * vpr + c);
+        }
+        dst_off[u] = dense * vpr + c;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+      if (dst_off[u] >= 0) __builtin_nontemporal_store(val[u], dst + dst_off[u]);
+  }
+}
+
+int vpr_log2(int vpr) {
+  for (int l = 0; l <= 8; ++l)
+    if (vpr == (1 << l)) return l;
+  return -1;
+}
+
+#define DASC_LAUNCH_BY_VPR(KERNEL, lg, grid, st, ...)                                   \
+  switch (lg) {                                                                         \
+    case 0: hipLaunchKernelGGL(KERNEL<0>, grid, dim3(kThreads), 0, st, __VA_ARGS__); break; \
+    case 1: hipLaunchKernelGGL(KERNEL<1>, grid, dim3(kThreads), 0, st, __VA_ARGS__); break; \
+    case 2: hipLaunchKernelGGL(KERNEL<2>, grid, dim3(kThreads), 0, st, __VA_ARGS__); break; \
+    case 3: hipLaunchKernelGGL(KERNEL<3>, grid, dim3(kThreads), 0, st, __VA_ARGS__); break; \
+    case 4: hipLaunchKernelGGL(KERNEL<4>, grid, dim3(kThreads), 0, st, __VA_ARGS__); break; \
+    case 5: hipLaunchKernelGGL(KERNEL<5>, grid, dim3(kThreads), 0, st, __VA_ARGS__); break; \
+    case 6: hipLaunchKernelGGL(KERNEL<6>, grid, dim3(kThreads), 0, st, __VA_ARGS__); break; \
+    case 7: hipLaunchKernelGGL(KERNEL<7>, grid, dim3(kThreads), 0, st, __VA_ARGS__); break; \
+    case 8: hipLaunchKernelGGL(KERNEL<8>, grid, dim3(kThreads), 0, st, __VA_ARGS__); break; \
+    default: hipLaunchKernelGGL(KERNEL<-1>, grid, dim3(kThreads), 0, st, __VA_ARGS__); break; \
+  }
+
+int check_common(const dasc_shape* shape, int64_t n_pool, int64_t n_ckpt_slots, int32_t n_ranks,
+                 int64_t slice_rows, int64_t n_rows, int32_t n) {
+  if (!dasc::valid_shape(shape)) return DASC_E_SHAPE;
+  if (shape->dv % 4 != 0) return DASC_E_SHAPE;
+  if (n < 0 || n_pool < 1 || n_ckpt_slots < 1 || n_ranks < 1 || n_rows < 0) return DASC_E_INVAL;
+  if (n_rows > dasc::rows_per_state(shape)) return DASC_E_SHAPE;
+  if (n_rows > 0 && (slice_rows < 1 || slice_rows > INT32_MAX || slice_rows * n_ranks < n_rows))
+    return DASC_E_INVAL;
+  return DASC_OK;
+}
+
+}  // namespace
+
+extern "C" int dasc_pack(const dasc_shape* shape, const float* states, int64_t n_pool,
+                         const int32_t* src_slot, const int32_t* unit_row, int64_t n_rows,
+                         float* ckpt, int64_t n_ckpt_slots, const int32_t* dst_slot,
+                         int32_t n_ranks, int64_t slice_rows, int32_t n, dasc_stream_t stream) {
+  int rc = check_common(shape, n_pool, n_ckpt_slots, n_ranks, slice_rows, n_rows, n);
+  if (rc != DASC_OK) return rc;
+  if (n == 0 || n_rows == 0) return DASC_OK;
+  if (!states || !src_slot || !unit_row || !ckpt || !dst_slot) return DASC_E_INVAL;
+  if (!dasc::aligned16(states) || !dasc::aligned16(ckpt)) return DASC_E_INVAL;
+  const int vpr = shape->dv / 4;
+  const int rpb = rows_per_block(vpr);
+  const int64_t bpc = (n_rows + rpb - 1) / rpb;
+  if (bpc * n > INT32_MAX) return DASC_E_INVAL;
+  (void)hipGetLastError();
+  DASC_LAUNCH_BY_VPR(pack_kernel, vpr_log2(vpr), dim3(unsigned(bpc * n)),
+                     reinterpret_cast<hipStream_t>(stream),
+                     reinterpret_cast<const f32x4*>(states), n_pool, dasc::rows_per_state(shape),
+                     src_slot, unit_row, n_rows, reinterpret_cast<f32x4*>(ckpt), n_ckpt_slots,
+                     dst_slot, slice_rows, int(bpc), rpb, vpr);
+  return dasc::launch_status();
+}
+
+extern "C" int dasc_restore(const dasc_shape* shape, const float* ckpt, int64_t n_ckpt_slots,
+                            const int32_t* src_slot, int32_t n_ranks, int64_t slice_rows,
+                            int64_t n_rows, const int32_t* inv_row, float* states,
+                            int64_t n_pool, const int32_t* dst_slot, int32_t n,
+                            dasc_stream_t stream) {
+  int rc = check_common(shape, n_pool, n_ckpt_slots, n_ranks, slice_rows, n_rows, n);
+  if (rc != DASC_OK) return rc;
+  if (n == 0) return DASC_OK;
+  if (!src_slot || !inv_row || !states || !dst_slot) return DASC_E_INVAL;
+  if (n_rows > 0 && !ckpt) return DASC_E_INVAL;
+  if (!dasc::aligned16(states) || !dasc::aligned16(ckpt)) return DASC_E_INVAL;
+  if (n_rows == 0) slice_rows = 1;  // nothing is read; keeps the divisor non-zero
+  const int vpr = shape->dv / 4;
+  const int rpb = rows_per_block(vpr);
+  const int64_t rows = dasc::rows_per_state(shape);
+  const int64_t bps = (rows + rpb - 1) / rpb;
+  if (bps * n > INT32_MAX) return DASC_E_INVAL;
+  (void)hipGetLastError();
+  DASC_LAUNCH_BY_VPR(restore_kernel, vpr_log2(vpr), dim3(unsigned(bps * n)),
+                     reinterpret_cast<hipStream_t>(stream),
+                     reinterpret_cast<const f32x4*>(ckpt), n_ckpt_slots, src_slot, slice_rows,
+                     n_rows, inv_row, reinterpret_cast<f32x4*>(states), n_pool, rows, dst_slot,
+                     int(bps), rpb, vpr);
+  return dasc::launch_status();
+}

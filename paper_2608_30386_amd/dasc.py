@@ -1,0 +1,209 @@
+"""Python binding of the DASC C ABI (argument marshalling only).
+
+Each function has the name of the C entry point it calls and does nothing but
+turn Python/NumPy/torch arguments into pointers and sizes: every step of the
+path runs in libdasc.so.  torch tensors supply device memory and the current
+HIP stream; host arrays for the planner are NumPy.
+
+Errors from the library raise DascError carrying the status code.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import _lib
+from ._lib import LIB
+
+ARCH = {"kda": _lib.DASC_ARCH_KDA, "gdn": _lib.DASC_ARCH_GDN}
+KEEP = {"threshold": _lib.DASC_KEEP_THRESHOLD, "topk_head": _lib.DASC_KEEP_TOPK_PER_HEAD,
+        "topk_layer": _lib.DASC_KEEP_TOPK_PER_LAYER}
+INIT = {"restored": _lib.DASC_INIT_RESTORED, "zero": _lib.DASC_INIT_ZERO}
+
+
+class DascError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {LIB.dasc_strerror(code).decode()} (status {code})")
+
+
+def _check(code: int, where: str) -> None:
+    if code != _lib.DASC_OK:
+        raise DascError(code, where)
+
+
+@dataclass(frozen=True)
+class Shape:
+    arch: str
+    n_layers: int
+    n_heads: int
+    n_qk_heads: int
+    dk: int
+    dv: int
+
+    def c(self) -> _lib.Shape:
+        return _lib.Shape(ARCH[self.arch], self.n_layers, self.n_heads, self.n_qk_heads,
+                          self.dk, self.dv)
+
+    @property
+    def rows(self) -> int:
+        return self.n_layers * self.n_heads * self.dk
+
+    @property
+    def units(self) -> int:
+        return self.rows if self.arch == "kda" else self.n_layers * self.n_heads
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+# ---- plan (host) ---------------------------------------------------------------
+
+def dasc_static_log_decay(a_log, dt_bias=None, a: float = -0.3) -> np.ndarray:
+    a_log = np.ascontiguousarray(a_log, dtype=np.float64)
+    out = np.empty_like(a_log)
+    dt = None if dt_bias is None else np.ascontiguousarray(
+        np.broadcast_to(dt_bias, a_log.shape), dtype=np.float64)
+    _check(LIB.dasc_static_log_decay(_ptr(a_log), None if dt is None else _ptr(dt), a,
+                                     a_log.size, _ptr(out)), "dasc_static_log_decay")
+    return out
+
+
+def dasc_plan(shape: Shape, g_static, keep_mode: str = "threshold", keep_k: int = 0,
+              w_max: int = 16, n_ranks: int = 1, eps: float = 1e-3, conv_bytes: int = 0) -> dict:
+    """Host planner; returns a dict of NumPy arrays and scalars (see dasc.h)."""
+    g = np.ascontiguousarray(g_static, dtype=np.float64)
+    desc = _lib.PlanDesc(shape.c(), KEEP[keep_mode], keep_k, w_max, n_ranks, eps, conv_bytes)
+    L, H, nu, rows, T = shape.n_layers, shape.n_heads, shape.units, shape.rows, n_ranks
+    arr = {
+        "keep": np.zeros(nu, np.uint8), "horizon": np.zeros(nu, np.float64),
+        "unit_count": np.zeros(L * H, np.int32), "off": np.zeros(L * H + 1, np.int32),
+        "layer_off": np.zeros(L + 1, np.int32), "unit_row": np.zeros(rows, np.int32),
+        "inv_row": np.zeros(rows, np.int32), "w_units": np.zeros(nu, np.int32),
+        "rank_begin": np.zeros(T + 1, np.int32), "send": np.zeros(T * T, np.int64),
+    }
+    out = _lib.PlanOut()
+    for name, a in arr.items():
+        setattr(out, name, a.ctypes.data_as(type(getattr(out, name))))
+    if g.size != nu:
+        raise ValueError(f"g_static has {g.size} entries, shape needs {nu}")
+    _check(LIB.dasc_plan(C.byref(desc), _ptr(g), C.byref(out)), "dasc_plan")
+    res = {k: getattr(out, k) for k, _ in _lib.PlanOut._fields_ if k not in arr}
+    unit_shape = (L, H, shape.dk) if shape.arch == "kda" else (L, H)
+    res.update({
+        "keep": arr["keep"].astype(bool).reshape(unit_shape),
+        "horizon": arr["horizon"].reshape(unit_shape),
+        "unit_count": arr["unit_count"].reshape(L, H),
+        "off": arr["off"], "layer_off": arr["layer_off"],
+        "unit_row": arr["unit_row"][: res["n_rows"]].copy(),
+        "inv_row": arr["inv_row"], "w_units": arr["w_units"].reshape(unit_shape),
+        "rank_begin": arr["rank_begin"], "send": arr["send"].reshape(T, T),
+    })
+    return res
+
+
+def dasc_matched_slots(budget_bytes: int, slot_bytes: int) -> int:
+    out = C.c_int64()
+    _check(LIB.dasc_matched_slots(budget_bytes, slot_bytes, C.byref(out)), "dasc_matched_slots")
+    return out.value
+
+
+# ---- device calls (torch tensors) ----------------------------------------------------
+
+def _dev(t, dtype, name):
+    import torch
+
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _need(t, n: int, name: str) -> None:
+    # The C ABI takes raw pointers; make sure the kernels stay inside each buffer.
+    if t.numel() < n:
+        raise ValueError(f"{name} has {t.numel()} elements, the call addresses {n}")
+
+
+def _stream(stream):
+    import torch
+
+    s = torch.cuda.current_stream() if stream is None else stream
+    return C.c_void_p(s.cuda_stream)
+
+
+def dasc_pack(shape: Shape, states, src_slot, unit_row, ckpt, dst_slot, n_ranks: int = 1,
+              slice_rows: int | None = None, stream=None) -> None:
+    """states [n_pool, L, H, dk, dv] f32 -> ckpt [T, n_slots, C_rows, dv] (or [n_slots, R, dv])."""
+    import torch
+
+    n_rows = unit_row.numel()
+    slice_rows = n_rows if slice_rows is None else slice_rows
+    n_slots = ckpt.shape[1] if ckpt.dim() == 4 else ckpt.shape[0]
+    _need(states, states.shape[0] * shape.rows * shape.dv, "states")
+    _need(ckpt, n_ranks * n_slots * slice_rows * shape.dv, "ckpt")
+    _need(dst_slot, src_slot.numel(), "dst_slot")
+    _check(LIB.dasc_pack(
+        C.byref(shape.c()), _dev(states, torch.float32, "states"), states.shape[0],
+        _dev(src_slot, torch.int32, "src_slot"), _dev(unit_row, torch.int32, "unit_row"), n_rows,
+        _dev(ckpt, torch.float32, "ckpt"), n_slots, _dev(dst_slot, torch.int32, "dst_slot"),
+        n_ranks, slice_rows, src_slot.numel(), _stream(stream)), "dasc_pack")
+
+
+def dasc_restore(shape: Shape, ckpt, src_slot, inv_row, states, dst_slot, n_rows: int,
+                 n_ranks: int = 1, slice_rows: int | None = None, stream=None) -> None:
+    import torch
+
+    slice_rows = n_rows if slice_rows is None else slice_rows
+    n_slots = ckpt.shape[1] if ckpt.dim() == 4 else ckpt.shape[0]
+    _need(states, states.shape[0] * shape.rows * shape.dv, "states")
+    _need(ckpt, n_ranks * n_slots * slice_rows * shape.dv, "ckpt")
+    _need(inv_row, shape.rows, "inv_row")
+    _need(dst_slot, src_slot.numel(), "dst_slot")
+    _check(LIB.dasc_restore(
+        C.byref(shape.c()), _dev(ckpt, torch.float32, "ckpt"), n_slots,
+        _dev(src_slot, torch.int32, "src_slot"), n_ranks, slice_rows, n_rows,
+        _dev(inv_row, torch.int32, "inv_row"), _dev(states, torch.float32, "states"),
+        states.shape[0], _dev(dst_slot, torch.int32, "dst_slot"), src_slot.numel(),
+        _stream(stream)), "dasc_restore")
+
+
+def dasc_refresh_workspace_bytes(shape: Shape, n_req: int, W: int) -> int:
+    out = C.c_size_t()
+    _check(LIB.dasc_refresh_workspace_bytes(C.byref(shape.c()), n_req, W, C.byref(out)),
+           "dasc_refresh_workspace_bytes")
+    return out.value
+
+
+def dasc_refresh(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta, W: int,
+                 init_mode: str = "restored", workspace=None, stream=None) -> None:
+    """Refresh one layer's omitted units for every request in `slot`.
+
+    k [n_req, Hqk, W, dk] and v [n_req, H, W, dv] are bfloat16 device tensors; g is
+    [n_req, H, W, dk] (KDA) or [n_req, H, W] (GDN) and beta [n_req, H, W], float32.
+    """
+    import torch
+
+    n_req, H, dk, dv = slot.numel(), shape.n_heads, shape.dk, shape.dv
+    _need(states, states.shape[0] * shape.rows * dv, "states")
+    _need(inv_row, shape.rows, "inv_row")
+    _need(k, n_req * shape.n_qk_heads * W * dk, "k")
+    _need(v, n_req * H * W * dv, "v")
+    _need(g, n_req * H * W * (dk if shape.arch == "kda" else 1), "g")
+    _need(beta, n_req * H * W, "beta")
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        ws_ptr, ws_bytes = _dev(workspace, torch.uint8, "workspace"), workspace.numel()
+    _check(LIB.dasc_refresh(
+        C.byref(shape.c()), layer, _dev(inv_row, torch.int32, "inv_row"),
+        _dev(states, torch.float32, "states"), states.shape[0], _dev(slot, torch.int32, "slot"),
+        _dev(k, torch.bfloat16, "k"), _dev(v, torch.bfloat16, "v"),
+        _dev(g, torch.float32, "g"), _dev(beta, torch.float32, "beta"),
+        slot.numel(), W, INIT[init_mode], ws_ptr, ws_bytes, _stream(stream)), "dasc_refresh")

@@ -1,0 +1,172 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects bad
+arguments with status codes before any launch (CPU only: no kernel runs)."""
+
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_30386_amd import _lib
+from paper_2608_30386_amd._lib import LIB, Shape, PlanDesc, PlanOut
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dasc.h")
+
+FAKE = C.c_void_p(0x10000)       # aligned, never dereferenced: validation fails first
+FAKE_ODD = C.c_void_p(0x10004)   # not 16-byte aligned
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:int|const char \*)\s*(dasc_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) == 8
+    assert set(names) == set(_lib.EXPORTED)
+    lib = C.CDLL(_lib.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_strerror_total():
+    for code in (0, -1, -2, -3, -4, -5, 7, -99):
+        assert LIB.dasc_strerror(code)
+
+
+def kda(L=2, H=4, Hqk=4, dk=16, dv=16):
+    return Shape(_lib.DASC_ARCH_KDA, L, H, Hqk, dk, dv)
+
+
+def pack(shape, n=1, states=FAKE, src=FAKE, unit_row=FAKE, n_rows=4, ckpt=FAKE, dst=FAKE,
+         n_pool=1, n_slots=1, T=1, slice_rows=4):
+    return LIB.dasc_pack(C.byref(shape) if shape is not None else None, states, n_pool, src,
+                         unit_row, n_rows, ckpt, n_slots, dst, T, slice_rows, n, None)
+
+
+def restore(shape, n=1, ckpt=FAKE, src=FAKE, inv=FAKE, states=FAKE, dst=FAKE, n_rows=4,
+            n_pool=1, n_slots=1, T=1, slice_rows=4):
+    return LIB.dasc_restore(C.byref(shape) if shape is not None else None, ckpt, n_slots, src, T,
+                            slice_rows, n_rows, inv, states, n_pool, dst, n, None)
+
+
+def test_pack_restore_argument_errors():
+    E = _lib
+    assert pack(None) == E.DASC_E_SHAPE
+    assert pack(kda(dv=6)) == E.DASC_E_SHAPE                     # dv % 4
+    assert pack(Shape(7, 1, 1, 1, 4, 4)) == E.DASC_E_SHAPE       # bad arch
+    assert pack(kda(H=4, Hqk=3)) == E.DASC_E_SHAPE               # H % Hqk
+    assert pack(kda(L=0)) == E.DASC_E_SHAPE
+    assert pack(kda(), n=-1) == E.DASC_E_INVAL
+    assert pack(kda(), n_pool=0) == E.DASC_E_INVAL
+    assert pack(kda(), n_rows=2 * 4 * 16 + 1) == E.DASC_E_SHAPE  # more rows than a state has
+    assert pack(kda(), T=2, slice_rows=1) == E.DASC_E_INVAL      # slices do not cover R
+    assert pack(kda(), states=None) == E.DASC_E_INVAL
+    assert pack(kda(), unit_row=None) == E.DASC_E_INVAL
+    assert pack(kda(), states=FAKE_ODD) == E.DASC_E_INVAL
+    assert pack(kda(), ckpt=FAKE_ODD) == E.DASC_E_INVAL
+    assert pack(kda(), n=0) == E.DASC_OK                         # nothing to do, no launch
+    assert pack(kda(), n_rows=0) == E.DASC_OK
+    assert restore(None) == E.DASC_E_SHAPE
+    assert restore(kda(), inv=None) == E.DASC_E_INVAL
+    assert restore(kda(), states=FAKE_ODD) == E.DASC_E_INVAL
+    assert restore(kda(), n_slots=0) == E.DASC_E_INVAL
+    assert restore(kda(), n=0) == E.DASC_OK
+
+
+def refresh(shape, layer=0, W=8, n_req=1, init=0, ptrs=None, ws=None, ws_bytes=0, n_pool=1):
+    p = dict(inv=FAKE, states=FAKE, slot=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE)
+    p.update(ptrs or {})
+    return LIB.dasc_refresh(C.byref(shape) if shape is not None else None, layer, p["inv"],
+                            p["states"], n_pool, p["slot"], p["k"], p["v"], p["g"], p["beta"],
+                            n_req, W, init, ws, ws_bytes, None)
+
+
+def test_refresh_argument_errors():
+    E = _lib
+    assert refresh(None) == E.DASC_E_INVAL
+    assert refresh(kda(dv=6)) == E.DASC_E_SHAPE
+    assert refresh(kda(), W=0) == E.DASC_E_INVAL
+    assert refresh(kda(), W=-3) == E.DASC_E_INVAL
+    assert refresh(kda(), layer=2) == E.DASC_E_INVAL
+    assert refresh(kda(), layer=-1) == E.DASC_E_INVAL
+    assert refresh(kda(), n_req=0) == E.DASC_E_INVAL
+    assert refresh(kda(), init=5) == E.DASC_E_INVAL
+    assert refresh(kda(), n_pool=0) == E.DASC_E_INVAL
+    for name in ("inv", "states", "slot", "k", "v", "g", "beta"):
+        assert refresh(kda(), ptrs={name: None}) == E.DASC_E_INVAL, name
+    assert refresh(kda(), ptrs={"states": FAKE_ODD}) == E.DASC_E_INVAL
+    assert refresh(kda(dk=8)) == E.DASC_E_UNSUPPORTED            # no kernel for dk = 8
+    assert refresh(kda(dv=512)) == E.DASC_E_UNSUPPORTED
+    gdn_bad = Shape(_lib.DASC_ARCH_GDN, 1, 4, 3, 16, 16)
+    assert refresh(gdn_bad) == E.DASC_E_SHAPE
+    need = C.c_size_t(99)
+    assert LIB.dasc_refresh_workspace_bytes(C.byref(kda()), 1, 0, C.byref(need)) == E.DASC_E_INVAL
+    assert LIB.dasc_refresh_workspace_bytes(C.byref(kda()), 2, 64, C.byref(need)) == E.DASC_OK
+
+
+def test_plan_argument_errors():
+    E = _lib
+    sh = kda(L=1, H=2, Hqk=2, dk=4, dv=4)
+    g = np.full(8, -0.5)
+    out = PlanOut()
+
+    def plan(desc, gg=g):
+        return LIB.dasc_plan(C.byref(desc), gg.ctypes.data, C.byref(out))
+
+    ok = PlanDesc(sh, 0, 0, 16, 1, 1e-3, 0)
+    assert plan(ok) == E.DASC_OK
+    assert LIB.dasc_plan(None, g.ctypes.data, C.byref(out)) == E.DASC_E_INVAL
+    assert LIB.dasc_plan(C.byref(ok), None, C.byref(out)) == E.DASC_E_INVAL
+    assert plan(PlanDesc(sh, 0, 0, 16, 1, 0.0, 0)) == E.DASC_E_INVAL        # eps
+    assert plan(PlanDesc(sh, 0, 0, 16, 1, 1.0, 0)) == E.DASC_E_INVAL
+    assert plan(PlanDesc(sh, 0, 0, -1, 1, 1e-3, 0)) == E.DASC_E_INVAL       # w_max
+    assert plan(PlanDesc(sh, 0, 0, 16, 0, 1e-3, 0)) == E.DASC_E_INVAL       # n_ranks
+    assert plan(PlanDesc(sh, 9, 0, 16, 1, 1e-3, 0)) == E.DASC_E_INVAL       # keep mode
+    assert plan(PlanDesc(sh, 1, 5, 16, 1, 1e-3, 0)) == E.DASC_E_INVAL       # k > dk
+    assert plan(PlanDesc(sh, 0, 0, 16, 1, 1e-3, -1)) == E.DASC_E_INVAL      # conv bytes
+    gdn = Shape(_lib.DASC_ARCH_GDN, 1, 2, 2, 4, 4)
+    assert plan(PlanDesc(gdn, 1, 1, 16, 1, 1e-3, 0), np.full(2, -0.5)) == E.DASC_E_SHAPE
+    for bad in (0.0, 0.3, np.inf, -np.inf, np.nan):
+        gb = g.copy()
+        gb[3] = bad
+        assert plan(ok, gb) == E.DASC_E_INVAL, bad
+    slots = C.c_int64()
+    assert LIB.dasc_matched_slots(100, 0, C.byref(slots)) == E.DASC_E_INVAL
+    assert LIB.dasc_matched_slots(-1, 10, C.byref(slots)) == E.DASC_E_INVAL
+    assert LIB.dasc_static_log_decay(None, None, -0.3, 1, g.ctypes.data) == E.DASC_E_INVAL
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    import paper_2608_30386_amd as D
+
+    sh = D.Shape("kda", 1, 2, 2, 16, 16)
+    x = torch.zeros(4)
+    with pytest.raises((TypeError, ValueError)):
+        D.dasc_pack(sh, x, x, x, x, x)
+    st = torch.zeros(1, 1, 2, 16, 16)
+    ck = torch.zeros(1, 1, 16)
+    idx = torch.zeros(1, dtype=torch.int32)
+    with pytest.raises(TypeError, match="device tensor"):
+        D.dasc_pack(sh, st, idx, idx, ck, idx)
+
+
+def test_code_independence():
+    """The library package and the oracle never import each other."""
+    pkg = os.path.join(ROOT, "paper_2608_30386_amd")
+    orc = os.path.join(ROOT, "oracle")
+    for d, bad in ((pkg, r"^\s*(from|import)\s+oracle\b"), (orc, r"paper_2608_30386_amd")):
+        for base, _, files in os.walk(d):
+            for f in files:
+                if f.endswith((".py", ".hip", ".cpp", ".h")):
+                    text = open(os.path.join(base, f)).read()
+                    assert not re.search(bad, text, re.M), (f, bad)
+    wl = os.path.join(ROOT, "workloads")
+    for f in os.listdir(wl):
+        if f.endswith(".py"):
+            text = open(os.path.join(wl, f)).read()
+            assert not re.search(r"^\s*(from|import)\s+(oracle|paper_2608_30386_amd)\b", text, re.M)

@@ -134,6 +134,7 @@ def test_refresh_writes_only_omitted_rows_and_shares_key_heads():
     g = (-0.3 * rng.uniform(0, 2, size=(n_req, H, W, dk))).astype(np.float32)
     beta = rng.uniform(0, 1, size=(n_req, H, W)).astype(np.float32)
     out, om = R.refresh(st, inv, kb, vb, g, beta, n_qk_heads=Hqk)
+    out = out.reshape(n_req, H, dk, dv)
     kept = ~om
     for n in range(n_req):
         for h in range(H):
@@ -142,10 +143,10 @@ def test_refresh_writes_only_omitted_rows_and_shares_key_heads():
     np.testing.assert_array_equal(out[:, [1, 3]], st[:, [1, 3]])
     # grouped key heads == the same keys duplicated per value head
     kdup = np.repeat(kb, H // Hqk, axis=1)
-    out2, _ = R.refresh(st, inv, kdup, vb, g, beta, n_qk_heads=H)
+    out2 = R.refresh(st, inv, kdup, vb, g, beta, n_qk_heads=H)[0].reshape(out.shape)
     np.testing.assert_array_equal(out, out2)
     # value head 2 must read key head 1: swapping key heads changes it
-    out3, _ = R.refresh(st, inv, kb[:, ::-1], vb, g, beta, n_qk_heads=Hqk)
+    out3 = R.refresh(st, inv, kb[:, ::-1], vb, g, beta, n_qk_heads=Hqk)[0].reshape(out.shape)
     assert not np.allclose(out3[:, 2], out[:, 2])
 
 
