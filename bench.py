@@ -1,0 +1,396 @@
+#!/usr/bin/env python3
+"""Benchmark of the DASC state-checkpoint hot path on one MI355X.
+
+One step = one pass of the whole device path over one batch of synthetic input:
+    pack     64 Kimi-Linear-shaped KDA layer states (32 heads, 128x128 fp32,
+             1556 of 4096 rows kept = 38%) into ragged checkpoints,
+    restore  the 64 checkpoints into fresh active states (omitted rows = +0.0),
+    refresh  16 of them by replaying W = 1024 suffix tokens of the gated delta
+             rule and overwriting only the omitted rows.
+The selection plan is built once on the host before timing (the paper builds it
+offline); its host time is reported separately.
+
+Prints one JSON line.  `value` is suffix tokens refreshed per second of whole-step
+time (n_req * W / step time); per-kernel rates are in `kernels`.  All inputs are
+resident in HBM before the timed region starts.
+
+    python bench.py [--steps K] [--warmup W] [--workload kimi_headline|kimi_model|qwen_gdn]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+FP32_VALU_PEAK_TFLOPS = 78.6    # 256 CU x 64 FMA lanes/clk x 2 FLOP x 2.4 GHz (no packed FP32)
+METRIC = "pack/restore GB/s + suffix-refresh tokens/s (KDA 32h x 128x128, W=1024)"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="kimi_headline",
+                    choices=["kimi_headline", "kimi_model", "qwen_gdn"])
+    ap.add_argument("--W", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="run only a plain device copy of known size (counter calibration)")
+    return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("pack_restore.hip", "refresh.hip", "launch_common.h"):
+        with open(os.path.join(ROOT, "paper_2608_30386_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch from the committed counter summary, if it matches this source."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("source_hash") != kernel_source_hash():
+        return None
+    return t.get("kernels", {}).get(kernel)
+
+
+class KernelTimer:
+    """HIP events around launches on the stream the library is given."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.spans = {}
+
+    def run(self, name, fn):
+        ev0 = self.torch.cuda.Event(enable_timing=True)
+        ev1 = self.torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        fn()
+        ev1.record()
+        self.spans.setdefault(name, []).append((ev0, ev1))
+
+    def mean_ms(self, name):
+        return float(np.mean([a.elapsed_time(b) for a, b in self.spans[name]]))
+
+
+def copy_calibration(torch):
+    n = 1 << 28  # 1 GiB of fp32
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 3}))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(the checkpoint kernels run on one device). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calib:
+        copy_calibration(torch)
+        return
+    if args.workload == "kimi_headline":
+        out = bench_headline(torch, args)
+    elif args.workload == "kimi_model":
+        out = bench_pack_restore_only(torch, args, "kimi_model")
+    else:
+        out = bench_gdn(torch, args)
+    print(json.dumps(out))
+
+
+# ---------------------------------------------------------------------------------------
+
+def _setup_plan(wl):
+    import paper_2608_30386_amd as D
+    from workloads import log_lambda
+
+    sh = D.Shape(wl.arch, wl.n_layers, wl.n_heads, wl.n_qk_heads, wl.dk, wl.dv)
+    t0 = time.perf_counter()
+    plan = D.dasc_plan(sh, D.dasc_static_log_decay(log_lambda(wl)), wl.keep_mode, wl.keep_k,
+                       wl.w_max, wl.n_ranks, wl.eps)
+    return sh, plan, time.perf_counter() - t0
+
+
+def _i32(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).cuda()
+
+
+def _bf16(torch, bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def bench_headline(torch, args):
+    import paper_2608_30386_amd as D
+    from workloads import WORKLOADS, log_lambda, refresh_inputs, states_host
+
+    wl = WORKLOADS["kimi_layer"]
+    W = args.W
+    n_ckpt, n_req = wl.n_ckpt, wl.n_req
+    sh, plan, plan_s = _setup_plan(wl)
+    R = int(plan["n_rows"])
+    rows, dv = sh.rows, sh.dv
+
+    states_np = states_host(wl, n_ckpt)
+    inp = refresh_inputs(wl, W, log_lambda(wl)[0])
+    states = torch.from_numpy(states_np).cuda()
+    ckpt = torch.empty((n_ckpt, R, dv), dtype=torch.float32, device="cuda")
+    active = torch.empty_like(states)
+    unit_row, inv_row = _i32(torch, plan["unit_row"]), _i32(torch, plan["inv_row"])
+    ids = _i32(torch, np.arange(n_ckpt))
+    req = _i32(torch, np.arange(n_req))
+    k, v = _bf16(torch, inp["k"]), _bf16(torch, inp["v"])
+    g, beta = torch.from_numpy(inp["g"]).cuda(), torch.from_numpy(inp["beta"]).cuda()
+    torch.cuda.synchronize()
+
+    timer = KernelTimer(torch)
+
+    def step():
+        timer.run("pack", lambda: D.dasc_pack(sh, states, ids, unit_row, ckpt, ids))
+        timer.run("restore", lambda: D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R))
+        timer.run("refresh", lambda: D.dasc_refresh(sh, 0, inv_row, active, req, k, v, g, beta, W))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    timer.spans.clear()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+
+    omitted = (plan["inv_row"] < 0).reshape(sh.n_heads, sh.dk)
+    heads_refreshed = int(omitted.any(axis=1).sum())
+    bytes_pack = 2 * R * dv * 4 * n_ckpt
+    bytes_restore = (R + rows) * dv * 4 * n_ckpt
+    # refresh reads k, v, g, beta and the restored state of every refreshed head, and
+    # writes the omitted rows
+    per_head = (2 * W * sh.dk + 2 * W * dv + 4 * W * sh.dk + 4 * W + 4 * sh.dk * dv)
+    bytes_refresh = n_req * (heads_refreshed * per_head + int(omitted.sum()) * dv * 4)
+    flops_refresh = 5.0 * sh.dk * dv * W * n_req * heads_refreshed   # decay, read-out, write
+
+    t = {n: timer.mean_ms(n) for n in ("pack", "restore", "refresh")}
+    kernels = {
+        "pack": {"ms": t["pack"], "GBps": bytes_pack / t["pack"] / 1e6,
+                 "hbm_frac": bytes_pack / t["pack"] / 1e6 / HBM_PEAK_GBPS, "bytes": bytes_pack},
+        "restore": {"ms": t["restore"], "GBps": bytes_restore / t["restore"] / 1e6,
+                    "hbm_frac": bytes_restore / t["restore"] / 1e6 / HBM_PEAK_GBPS,
+                    "bytes": bytes_restore},
+        "refresh": {"ms": t["refresh"], "tokens_per_s": n_req * W / (t["refresh"] / 1e3),
+                    "GBps": bytes_refresh / t["refresh"] / 1e6,
+                    "TFLOPs": flops_refresh / t["refresh"] / 1e9, "bytes": bytes_refresh,
+                    "flops": flops_refresh, "heads": n_req * heads_refreshed},
+    }
+    achieved = flops_refresh / (t["refresh"] / 1e3) / 1e12
+    traffic = measured_traffic("refresh")
+    out = {
+        "metric": METRIC,
+        "value": n_req * W / (ms_step / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"KDA layer 32h x 128x128 fp32: pack+restore {n_ckpt} checkpoints "
+                        f"(R={R} of {rows} rows kept), refresh {n_req} requests W={W}",
+            "n_checkpoints": n_ckpt, "n_requests": n_req, "W": W, "rows_kept": R,
+            "inputs": "k,v bf16; g,beta fp32; state fp32",
+        },
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": FP32_VALU_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / FP32_VALU_PEAK_TFLOPS,
+                     "traffic": traffic, "kernel": "refresh",
+                     "work_per_launch": f"{flops_refresh:.4g} FLOP = 5*dk*dv per head-token"},
+        "kernels": kernels,
+        "pack_restore_GBps": (bytes_pack + bytes_restore) / (t["pack"] + t["restore"]) / 1e6,
+        "plan_host_ms": plan_s * 1e3,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_headline(wl, plan, states_np, inp, W, n_req)
+    return out
+
+
+def cpu_baseline_headline(wl, plan, states_np, inp, W, n_req):
+    """The oracle, as it stands, on a bounded sample of the same step."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import pack as OK
+    from oracle import recurrence as OR
+
+    n_s, req_s = 8, 2                         # 8 of 64 checkpoints, 2 of 16 requests
+    R = int(plan["n_rows"])
+    words = states_np.reshape(states_np.shape[0], -1, wl.dv).view(np.uint32)
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        ck = OK.pack(words, list(range(n_s)), plan["unit_row"],
+                     np.zeros((1, n_s, R, wl.dv), np.uint32), list(range(n_s)))
+        t_pack = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        back = OK.restore(ck, list(range(n_s)), plan["unit_row"], np.zeros_like(words[:n_s]),
+                          list(range(n_s)))
+        t_restore = time.perf_counter() - t0
+        layer = back.view(np.float32).reshape(n_s, wl.n_heads, wl.dk, wl.dv)
+        pairs = [(n, h) for n in range(req_s) for h in range(wl.n_heads)]
+        sub = {key: val[:req_s] for key, val in inp.items()}
+        t0 = time.perf_counter()
+        OR.refresh(layer[:req_s], plan["inv_row"], sub["k"], sub["v"], sub["g"], sub["beta"],
+                   wl.n_qk_heads, pairs=pairs)
+        t_ref = time.perf_counter() - t0
+    scale_ck = wl.n_ckpt / n_s
+    step_s = (t_pack + t_restore) * scale_ck + t_ref * n_req / req_s
+    return {"value": n_req * W / step_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"pack+restore {n_s} of {wl.n_ckpt} checkpoints, refresh {req_s} of "
+                      f"{n_req} requests (all 32 heads, W={W}, fp64 per-token form); "
+                      "scaled linearly to the full step",
+            "sample_seconds": t_pack + t_restore + t_ref,
+            "host_cpus": os.cpu_count()}
+
+
+def bench_pack_restore_only(torch, args, name):
+    """GB-scale pack + restore (full-model KDA set) for the HBM roofline."""
+    import paper_2608_30386_amd as D
+    from workloads import WORKLOADS, states_device
+
+    wl = WORKLOADS[name]
+    sh, plan, plan_s = _setup_plan(wl)
+    R, rows, dv, n = int(plan["n_rows"]), sh.rows, sh.dv, wl.n_ckpt
+    T, C = wl.n_ranks, int(plan["slice_rows"])
+    states = states_device(wl, n, "cuda")
+    ckpt = torch.empty((T, n, C, dv), dtype=torch.float32, device="cuda")
+    active = torch.empty_like(states)
+    unit_row, inv_row = _i32(torch, plan["unit_row"]), _i32(torch, plan["inv_row"])
+    ids = _i32(torch, np.arange(n))
+    timer = KernelTimer(torch)
+
+    def step():
+        timer.run("pack", lambda: D.dasc_pack(sh, states, ids, unit_row, ckpt, ids, n_ranks=T,
+                                              slice_rows=C))
+        timer.run("restore", lambda: D.dasc_restore(sh, ckpt, ids, inv_row, active, ids,
+                                                    n_rows=R, n_ranks=T, slice_rows=C))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    timer.spans.clear()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    bp = 2 * R * dv * 4 * n
+    br = (R + rows) * dv * 4 * n
+    t = {k_: timer.mean_ms(k_) for k_ in ("pack", "restore")}
+    gbps = (bp + br) / (t["pack"] + t["restore"]) / 1e6
+    dom = "restore" if t["restore"] >= t["pack"] else "pack"
+    dom_bytes = br if dom == "restore" else bp
+    ach = dom_bytes / t[dom] / 1e6
+    return {
+        "metric": "pack+restore GB/s (full-model KDA checkpoint set)", "value": gbps, "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.n_layers} KDA layers x 32h x 128x128 fp32, {n} checkpoints, "
+                               f"R={R} of {rows} rows kept, T={T} rank slices"},
+        "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": ach / HBM_PEAK_GBPS, "traffic": measured_traffic(dom), "kernel": dom},
+        "kernels": {k_: {"ms": t[k_], "GBps": b / t[k_] / 1e6, "hbm_frac": b / t[k_] / 1e6 / HBM_PEAK_GBPS,
+                         "bytes": b} for k_, b in (("pack", bp), ("restore", br))},
+        "plan_host_ms": plan_s * 1e3,
+    }
+
+
+def bench_gdn(torch, args):
+    """Qwen-GDN shape: pack/restore 128 checkpoints, refresh 8 requests x 36 layers."""
+    import paper_2608_30386_amd as D
+    from workloads import WORKLOADS, log_lambda, refresh_inputs, states_device
+
+    wl = WORKLOADS["qwen_gdn"]
+    sh, plan, plan_s = _setup_plan(wl)
+    R, rows, dv, n, W = int(plan["n_rows"]), sh.rows, sh.dv, wl.n_ckpt, args.W
+    states = states_device(wl, n, "cuda")
+    ckpt = torch.empty((n, R, dv), dtype=torch.float32, device="cuda")
+    active = torch.empty_like(states)
+    unit_row, inv_row = _i32(torch, plan["unit_row"]), _i32(torch, plan["inv_row"])
+    ids, req = _i32(torch, np.arange(n)), _i32(torch, np.arange(wl.n_req))
+    lam = log_lambda(wl)
+    layers = []
+    for l in range(wl.n_layers):
+        inp = refresh_inputs(wl, W, lam[l], salt=l)
+        layers.append((_bf16(torch, inp["k"]), _bf16(torch, inp["v"]),
+                       torch.from_numpy(inp["g"]).cuda(), torch.from_numpy(inp["beta"]).cuda()))
+    timer = KernelTimer(torch)
+
+    def step():
+        timer.run("pack", lambda: D.dasc_pack(sh, states, ids, unit_row, ckpt, ids))
+        timer.run("restore", lambda: D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R))
+
+        def ref():
+            for l, (k, v, g, b) in enumerate(layers):
+                D.dasc_refresh(sh, l, inv_row, active, req, k, v, g, b, W)
+        timer.run("refresh_all_layers", ref)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    timer.spans.clear()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    t = {k_: timer.mean_ms(k_) for k_ in ("pack", "restore", "refresh_all_layers")}
+    bp, br = 2 * R * dv * 4 * n, (R + rows) * dv * 4 * n
+    om_heads = int((plan["inv_row"].reshape(-1, sh.dk) < 0).all(axis=1).sum())
+    heads = wl.n_req * om_heads
+    per_head = 2 * W * sh.dk + 2 * W * dv + 4 * W + 4 * W + 4 * sh.dk * dv   # k, v, g, beta, write
+    flops = 5.0 * sh.dk * dv * W * heads
+    ach = flops / (t["refresh_all_layers"] / 1e3) / 1e12
+    return {
+        "metric": "GDN pack/restore GB/s + refresh tokens/s (36 layers)",
+        "value": wl.n_req * W / (t["refresh_all_layers"] / 1e3), "unit": "tokens/s (all 36 layers)",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"Qwen-GDN 36 layers 16 qk / 32 v heads 128x128: pack+restore {n} "
+                               f"checkpoints (12 of 32 heads kept), refresh {wl.n_req} requests x "
+                               f"{om_heads} omitted heads W={W}"},
+        "roofline": {"bound": "alu", "achieved": ach, "peak": FP32_VALU_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": ach / FP32_VALU_PEAK_TFLOPS, "traffic": None,
+                     "kernel": "refresh"},
+        "kernels": {"pack": {"ms": t["pack"], "GBps": bp / t["pack"] / 1e6},
+                    "restore": {"ms": t["restore"], "GBps": br / t["restore"] / 1e6},
+                    "refresh_all_layers": {"ms": t["refresh_all_layers"],
+                                           "GBps": heads * per_head / t["refresh_all_layers"] / 1e6}},
+        "plan_host_ms": plan_s * 1e3,
+    }
+
+
+if __name__ == "__main__":
+    main()

@@ -57,12 +57,30 @@ class PlanOut(C.Structure):
     ]
 
 
+def _hip_runtimes() -> set:
+    paths = set()
+    with open("/proc/self/maps") as fh:
+        for line in fh:
+            if "libamdhip64" in line:
+                paths.add(os.path.realpath(line.split()[-1]))
+    return paths
+
+
 def _load() -> C.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(
             f"{LIB_PATH} is missing: build it with `python -m paper_2608_30386_amd.build` "
             "(there is no non-HIP fallback)")
+    # torch supplies device memory and streams, so the library must run on torch's HIP
+    # runtime: load torch first, and libdasc.so then binds to the libamdhip64 already
+    # in the process instead of mapping a second runtime that would not know torch's
+    # streams.
+    import torch  # noqa: F401
+
     lib = C.CDLL(LIB_PATH)
+    rts = _hip_runtimes()
+    if len(rts) > 1:
+        raise ImportError(f"two HIP runtimes are mapped in this process: {sorted(rts)}")
     P, I32, I64, SZ, D = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t, C.c_double
     sig = {
         "dasc_static_log_decay": [P, P, D, I64, P],
