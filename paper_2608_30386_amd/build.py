@@ -21,7 +21,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdasc.so")
 
-HIP_SOURCES = ["pack_restore.hip", "refresh.hip"]
+HIP_SOURCES = ["pack_restore.hip", "refresh.hip", "refresh_wy.hip"]
 HOST_SOURCES = ["plan.cpp"]
 ARCH = "gfx950"
 

@@ -17,9 +17,12 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <cstdlib>
+#include <cstring>
 
 #include "dasc.h"
 #include "launch_common.h"
+#include "refresh_kernels.h"
 
 namespace {
 
@@ -148,6 +151,16 @@ extern "C" int dasc_refresh(const dasc_shape* shape, int32_t layer, const int32_
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int zero = init_mode == DASC_INIT_ZERO;
   (void)hipGetLastError();
+  // The chunked MFMA kernel serves dk = dv = 128; every other shape, or an explicit
+  // DASC_REFRESH_KERNEL=column, takes the per-column fp32 kernel.
+  const char* pick = std::getenv("DASC_REFRESH_KERNEL");
+  const bool force_column = pick && std::strcmp(pick, "column") == 0;
+  if (!force_column && dasc::refresh_wy_supported(dk, dv)) {
+    dasc::launch_refresh_wy(per_channel, n_req, shape->n_heads, shape->n_qk_heads, layer,
+                            shape->n_layers, inv_row, states, n_pool, slot, k, v, g, beta, W,
+                            zero, st);
+    return dasc::launch_status();
+  }
   switch (dk) {
 #define DASC_DK(D)                                                                              \
   case D:                                                                                       \

@@ -1,0 +1,17 @@
+// Internal launchers of the refresh kernels (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace dasc {
+
+// Chunkwise WY-form kernel on bf16 MFMA; built for dk = dv = 128 only.
+bool refresh_wy_supported(int dk, int dv);
+void launch_refresh_wy(bool per_channel, int n_req, int H, int Hqk, int layer, int L,
+                       const int32_t* inv_row, float* states, int64_t n_pool, const int32_t* slot,
+                       const uint16_t* k, const uint16_t* v, const float* g, const float* beta,
+                       int W, int init_zero, hipStream_t st);
+
+}  // namespace dasc

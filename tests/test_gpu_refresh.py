@@ -154,3 +154,66 @@ def test_ragged_shapes(arch, dk, dv, H, Hqk, W):
         got = run_refresh(sh, pool, 1, inv, inp, W, init, slots=slots)
         pairs = [(n, h) for n in range(n_req) for h in range(H)]
         check(sh, pool, got, 1, inv, inp, pairs, init, slots=slots)
+
+
+def _inputs_128(arch, n_req, H, Hqk, W, seed, g_lo=None):
+    rng = np.random.default_rng(seed)
+    dk = dv = 128
+    k = rng.standard_normal((n_req, Hqk, W, dk)).astype(np.float32)
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    gshape = (n_req, H, W, dk) if arch == "kda" else (n_req, H, W)
+    lam = np.exp(rng.uniform(math.log(1e-4), 0, size=gshape[:2] + (1,) * (len(gshape) - 2)))
+    g = -lam * np.logaddexp(0, rng.standard_normal(gshape))
+    if g_lo is not None:        # plant very strong decays on a few tokens
+        m = rng.random(gshape) < 0.05
+        g = np.where(m, rng.uniform(g_lo, -8.0, size=gshape), g)
+    return {
+        "k": bf16_bits_from_f32(k),
+        "v": bf16_bits_from_f32(rng.standard_normal((n_req, H, W, dv)).astype(np.float32)),
+        "g": g.astype(np.float32),
+        "beta": (1 / (1 + np.exp(-rng.standard_normal((n_req, H, W))))).astype(np.float32),
+    }
+
+
+@pytest.mark.parametrize("arch,W,g_lo", [
+    ("kda", 1, None), ("kda", 31, None), ("kda", 33, None), ("kda", 100, None),
+    ("kda", 64, -30.0), ("gdn", 47, None), ("gdn", 96, -30.0),
+])
+def test_chunked_kernel_ragged_and_strong_decay(arch, W, g_lo):
+    # dk = dv = 128 takes the chunked MFMA kernel; ragged last chunks and very strong
+    # decays (floored at -10 inside the kernel) must stay within the bar
+    L, H, Hqk, n_req = 1, 4, 2, 3
+    sh = D.Shape(arch, L, H, Hqk, 128, 128)
+    rng = np.random.default_rng(W)
+    unit_shape = (L, H, 128) if arch == "kda" else (L, H)
+    g_static = D.dasc_static_log_decay(rng.uniform(math.log(1e-4), 0, size=unit_shape))
+    g_static[0, 0] = math.log(1e-3) / 2.0
+    plan = D.dasc_plan(sh, g_static, "threshold", 0, 64)
+    inv = plan["inv_row"]
+    pool = (0.05 * rng.standard_normal((4, L, H, 128, 128))).astype(np.float32)
+    pool.reshape(4, -1, 128)[:, inv < 0] = 0.0
+    inp = _inputs_128(arch, n_req, H, Hqk, W, seed=W, g_lo=g_lo)
+    slots = [3, 1, 0]
+    for init in ("restored", "zero"):
+        got = run_refresh(sh, pool, 0, inv, inp, W, init, slots=slots)
+        pairs = [(n, h) for n in range(n_req) for h in range(H)]
+        err = check(sh, pool, got, 0, inv, inp, pairs, init, slots=slots)
+        announce(f"chunked {arch} W={W} g_lo={g_lo} init={init} max rel err {err:.2e}")
+
+
+def test_chunked_and_column_kernels_agree(monkeypatch):
+    wl = WORKLOADS["kimi_layer"]
+    lib, _ = plans(wl)
+    sh = shape_of(wl)
+    n_req = 4
+    pool = restored_states(wl, lib, n_req)
+    inp = refresh_inputs(wl, 160, log_lambda(wl)[0], n_req=n_req)
+    a = run_refresh(sh, pool, 0, lib["inv_row"], inp, 160)
+    monkeypatch.setenv("DASC_REFRESH_KERNEL", "column")
+    b = run_refresh(sh, pool, 0, lib["inv_row"], inp, 160)
+    om = lib["inv_row"] < 0
+    diff = np.abs(a.reshape(n_req, -1, 128)[:, om] - b.reshape(n_req, -1, 128)[:, om]).max()
+    scale = np.abs(b.reshape(n_req, -1, 128)[:, om]).max()
+    announce(f"chunked vs column max diff / max {diff / scale:.2e}")
+    assert diff <= 1e-3 * scale
+    assert np.array_equal(a.reshape(n_req, -1, 128)[:, ~om], b.reshape(n_req, -1, 128)[:, ~om])
