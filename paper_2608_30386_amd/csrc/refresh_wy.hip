@@ -5,29 +5,31 @@
 // Unrolled over a chunk of C = 32 tokens with G_t = sum_{r<=t} g_r (per channel):
 //     A_ts = beta_t sum_c k_tc k_sc exp(G_tc - G_sc)      (s < t)
 //     T    = (I + A)^{-1},   T' = T Diag(beta)
-//     U    = T' V - (T' K_G) S'          K_G = k * exp(G)          (per-token deltas)
+//     U    = T' (V - K_G S')          K_G = k * exp(G)         (per-token deltas)
 //     S'  <- Diag(exp(G_C)) S' + K_H^T U   K_H = k * exp(G_C - G)
 // which is the per-token rule exactly, up to rounding.
 //
 // Work split: one 256-thread block per (request, head); wave w owns value columns
 // [32w, 32w + 32) of S' (128 x 32 fp32 = 16 MFMA accumulator tiles held in VGPRs for
-// the whole replay).  The per-chunk quantities that do not depend on S' (cumulative
-// decays, A, T', T' K_G, K_H) are built cooperatively in LDS; then each wave runs
-// the two state contractions on its columns.
+// the whole replay).  Everything that does not depend on S' (cumulative decays, K_G,
+// K_H, A, T') is built cooperatively in LDS each chunk; then each wave runs its three
+// chained contractions K_G S', T'(V - .), K_H^T U on its own columns.
 //
 // Precision.  Every product runs on v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
 // An fp32 operand x is split into x_hi = bf16(x) and x_lo = bf16(x - x_hi); a product
-// is formed as a_hi b_hi + a_lo b_hi + a_hi b_lo, which keeps ~16 mantissa bits per
-// term (exact bf16 inputs such as v skip the split).  This is what lets an fp32 state
-// survive thousands of tokens within 2e-3 while running at bf16 matrix-core rate.
+// is formed as a_lo b_hi + a_hi b_lo + a_hi b_hi, which keeps ~16 mantissa bits per
+// term.  This is what lets an fp32 state survive thousands of tokens within 2e-3 while
+// running at the bf16 matrix-core rate.
 //
 // Register-resident chaining.  In the 16x16x32 layout lane (q = lane/16, r = lane%16)
 // holds A[m = r][k = 8q + e], B[k = 8q + e][n = r] and D[m = 4q + i][n = r].  The
-// contraction index k can be any bijection shared by A and B, so the state tiles
-// (D layout: rows 4q + i) are fed straight back as B operands by taking
-// k(q, e) = 4q + e (e < 4) and 16 + 4q + (e - 4) (e >= 4) over a pair of 16-row tiles;
-// the LDS-side operand is read with the same mapping.  Neither S' nor U ever leaves
-// registers.
+// contraction index can be any bijection shared by A and B, so an accumulator pair of
+// 16-row tiles is fed straight back as a B operand by taking k(q, e) = 4q + e (e < 4)
+// and 16 + 4q + (e - 4) (e >= 4); the LDS-side operand is read with the same mapping.
+// S', K_G S', V - K_G S' and U never leave registers.
+//
+// LDS rows are padded so that the 16 (or 32) rows touched by one access instruction
+// fall on distinct banks; every operand is read as a 16- or 8-byte vector.
 //
 // Decay factors.  exp(G_t - G_s) <= 1 for s <= t, but the factorised form needs
 // exp(G_t - G_ref) exp(G_ref - G_s).  Off-diagonal 16-token blocks use the block
@@ -52,28 +54,35 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int C = 32;       // tokens per chunk
 constexpr int D = 128;      // dk = dv
 constexpr float kGateFloor = -10.f;
+constexpr float kLog2e = 1.4426950408889634f;
 
-// LDS map (bytes).  G is dead once the A tiles and K_G/K_H are built, and its space
-// then holds -T'K_G.
-constexpr int OFF_G = 0;            // f32 [C][D] cumulative log-decay
-constexpr int OFF_WNH = 0;          // bf16 [C][D] -(T'K_G), hi part
-constexpr int OFF_WNL = 8192;       // bf16 [C][D] lo part
-constexpr int OFF_KRAW = 16384;     // bf16 [C][D] keys of the chunk
-constexpr int OFF_VT = 24576;       // bf16 [D][C] values, transposed
-constexpr int OFF_KGH = 32768;      // bf16 [D][C] K_G^T hi
-constexpr int OFF_KGL = 40960;      // bf16 [D][C] K_G^T lo
-constexpr int OFF_KHH = 49152;      // bf16 [D][C] K_H^T hi
-constexpr int OFF_KHL = 57344;      // bf16 [D][C] K_H^T lo
-constexpr int OFF_AM = 65536;       // f32 [C][C] A
-constexpr int OFF_TM = 69632;       // f32 [C][C] T
-constexpr int OFF_Y = 73728;        // f32 [16][16] A10 T00
-constexpr int OFF_TPH = 74752;      // bf16 [C][C] T' hi
-constexpr int OFF_TPL = 76800;      // bf16 [C][C] T' lo
-constexpr int OFF_BETA = 78848;     // f32 [C]
-constexpr int OFF_GAM = 78976;      // f32 [D] exp(G_C)
-constexpr int LDS_BYTES = 79488;
+// padded row strides (elements)
+constexpr int SG = 132;     // f32 [C][SG]   cumulative log2-decay
+constexpr int SK = 136;     // bf16 [C][SK]  keys, K_G
+constexpr int SV = 40;      // bf16 [D][SV]  values transposed, K_H^T
+constexpr int SP = 36;      // bf16 [C][SP]  T' (8-byte aligned rows)
+
+// LDS map (bytes).  The key buffer is dead once A and K_H are built and then holds
+// T and T'.
+constexpr int OFF_G = 0;                       // f32  [C][SG]
+constexpr int OFF_K = OFF_G + C * SG * 4;      // bf16 [C][SK]  -> later T, T'
+constexpr int OFF_T = OFF_K;                   // f32  [C][C]
+constexpr int OFF_TPH = OFF_K + C * C * 4;     // bf16 [C][SP]
+constexpr int OFF_TPL = OFF_TPH + C * SP * 2;
+constexpr int OFF_VT = OFF_K + C * SK * 2;     // bf16 [D][SV]
+constexpr int OFF_KGH = OFF_VT + D * SV * 2;   // bf16 [C][SK]
+constexpr int OFF_KGL = OFF_KGH + C * SK * 2;
+constexpr int OFF_KHH = OFF_KGL + C * SK * 2;  // bf16 [D][SV]
+constexpr int OFF_KHL = OFF_KHH + D * SV * 2;
+constexpr int OFF_A = OFF_KHL + D * SV * 2;    // f32  [C][C]
+constexpr int OFF_BETA = OFF_A + C * C * 4;    // f32  [C]
+constexpr int OFF_GAM = OFF_BETA + C * 4;      // f32  [D] exp(G_C)
+constexpr int LDS_BYTES = OFF_GAM + D * 4;
+static_assert(C * C * 4 + 2 * C * SP * 2 <= C * SK * 2, "T and T' must fit in the key buffer");
+static_assert(LDS_BYTES <= 81920, "two blocks per CU");
 
 __device__ inline float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
+__device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ inline void split(float x, __bf16& hi, __bf16& lo) {
   hi = static_cast<__bf16>(x);
@@ -91,6 +100,10 @@ __device__ inline f32x4 mma3(bf16x8 ah, bf16x8 al, bf16x8 bh, bf16x8 bl, f32x4 c
   return mma(ah, bh, c);
 }
 
+__device__ inline f32x4 mma32(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
 __device__ inline bf16x8 cat(bf16x4 a, bf16x4 b) {
   return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
 }
@@ -103,17 +116,14 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     const float* __restrict__ beta, int W, int init_zero) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
   float* sG = reinterpret_cast<float*>(smem + OFF_G);
-  __bf16* sWNH = reinterpret_cast<__bf16*>(smem + OFF_WNH);
-  __bf16* sWNL = reinterpret_cast<__bf16*>(smem + OFF_WNL);
-  uint16_t* sK = reinterpret_cast<uint16_t*>(smem + OFF_KRAW);
+  uint16_t* sK = reinterpret_cast<uint16_t*>(smem + OFF_K);
+  float* sT = reinterpret_cast<float*>(smem + OFF_T);
   uint16_t* sVT = reinterpret_cast<uint16_t*>(smem + OFF_VT);
   __bf16* sKGH = reinterpret_cast<__bf16*>(smem + OFF_KGH);
   __bf16* sKGL = reinterpret_cast<__bf16*>(smem + OFF_KGL);
   __bf16* sKHH = reinterpret_cast<__bf16*>(smem + OFF_KHH);
   __bf16* sKHL = reinterpret_cast<__bf16*>(smem + OFF_KHL);
-  float* sA = reinterpret_cast<float*>(smem + OFF_AM);
-  float* sT = reinterpret_cast<float*>(smem + OFF_TM);
-  float* sY = reinterpret_cast<float*>(smem + OFF_Y);
+  float* sA = reinterpret_cast<float*>(smem + OFF_A);
   __bf16* sTPH = reinterpret_cast<__bf16*>(smem + OFF_TPH);
   __bf16* sTPL = reinterpret_cast<__bf16*>(smem + OFF_TPL);
   float* sBeta = reinterpret_cast<float*>(smem + OFF_BETA);
@@ -149,110 +159,134 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   const float* gp = PER_CHANNEL ? g + (int64_t(n) * H + h) * W * D : g + (int64_t(n) * H + h) * W;
   const float* bp = beta + (int64_t(n) * H + h) * W;
 
-  const int ch = tid & (D - 1);   // channel owned in the decay phases
+  const int ch = tid & (D - 1);   // channel (or value column) owned in the load phases
   const int hf = tid >> 7;        // which 16-token half of the chunk
+
+  // Gates, keys and beta of one chunk as this thread loads them.  Loads are
+  // unconditional (index clamped to the last valid token, value masked when consumed)
+  // so that all of them are in flight together; the next chunk's are issued one chunk
+  // ahead.  Values are loaded at the top of each chunk (registers are the limit).
+  float graw[16];
+  uint4 kraw[2];
+  float braw;
+  auto fetch = [&](int c0, int nvalid) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int tc = c0 + min(16 * hf + i, nvalid - 1);
+      graw[i] = PER_CHANNEL ? gp[int64_t(tc) * D + ch] : gp[tc];
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
+      kraw[u] = *reinterpret_cast<const uint4*>(kp + int64_t(c0 + min(t, nvalid - 1)) * D + c8);
+    }
+    braw = bp[c0 + min(tid & (C - 1), nvalid - 1)];
+  };
+  fetch(0, min(C, W));
 
   for (int t0 = 0; t0 < W; t0 += C) {
     const int nv = min(C, W - t0);  // valid tokens; the rest are zero (identity) tokens
 
-    // ---- load: gates -> cumulative decay, keys, values (transposed), beta ------------
+    // ---- values of this chunk (issued first), then the prefetched gates, keys, beta ---
+    uint16_t vraw[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) vraw[i] = vp[int64_t(t0 + min(16 * hf + i, nv - 1)) * D + ch];
     float Gl[16];
     {
       float run = 0.f;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const int t = 16 * hf + i;
-        float gv = 0.f;
-        if (t < nv) gv = PER_CHANNEL ? gp[int64_t(t0 + t) * D + ch] : gp[t0 + t];
-        run += fmaxf(gv, kGateFloor);
+        const float gv = 16 * hf + i < nv ? graw[i] : 0.f;
+        run += fmaxf(gv, kGateFloor) * kLog2e;
         Gl[i] = run;
       }
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int e = tid + 256 * u;
-      const int t = e >> 4, c8 = (e & 15) * 8;
-      uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-      if (t < nv) {
-        kv = *reinterpret_cast<const uint4*>(kp + int64_t(t0 + t) * D + c8);
-        vv = *reinterpret_cast<const uint4*>(vp + int64_t(t0 + t) * D + c8);
-      }
-      *reinterpret_cast<uint4*>(sK + t * D + c8) = kv;
-      const uint32_t vw[4] = {vv.x, vv.y, vv.z, vv.w};
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        sVT[(c8 + 2 * x) * C + t] = uint16_t(vw[x] & 0xFFFF);
-        sVT[(c8 + 2 * x + 1) * C + t] = uint16_t(vw[x] >> 16);
-      }
+      const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
+      *reinterpret_cast<uint4*>(sK + t * SK + c8) = t < nv ? kraw[u] : make_uint4(0, 0, 0, 0);
     }
-    if (tid < C) sBeta[tid] = tid < nv ? bp[t0 + tid] : 0.f;
+    {  // value column ch, tokens 16hf .. 16hf+15 -> one transposed row segment
+      uint32_t pk[8];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) sG[(16 * hf + i) * D + ch] = Gl[i];
+      for (int i = 0; i < 16; i += 2) {
+        const int t = 16 * hf + i;
+        const uint32_t a = t < nv ? vraw[i] : 0u;
+        const uint32_t b = t + 1 < nv ? vraw[i + 1] : 0u;
+        pk[i >> 1] = a | (b << 16);
+      }
+      uint4* dst = reinterpret_cast<uint4*>(sVT + ch * SV + 16 * hf);
+      dst[0] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+      dst[1] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
+    }
+    if (tid < C) sBeta[tid] = tid < nv ? braw : 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sG[(16 * hf + i) * SG + ch] = Gl[i];
     __syncthreads();
     if (hf == 1) {
-      const float base = sG[15 * D + ch];
+      const float base = sG[15 * SG + ch];
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         Gl[i] += base;
-        sG[(16 + i) * D + ch] = Gl[i];
+        sG[(16 + i) * SG + ch] = Gl[i];
       }
-      sGam[ch] = __expf(Gl[15]);
+      sGam[ch] = ex2(Gl[15]);
     }
     __syncthreads();
 
-    // ---- K_G^T = (k exp(G))^T and K_H^T = (k exp(G_C - G))^T, split hi/lo ----------
-    {
-      const float gC = sG[31 * D + ch];
-      bf16x8 gh[2], gl[2], hh[2], hl[2];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float kv = bf2f(sK[(16 * hf + i) * D + ch]);
-        __bf16 a, b;
-        split(kv * __expf(Gl[i]), a, b);
-        gh[i >> 3][i & 7] = a;
-        gl[i >> 3][i & 7] = b;
-        split(kv * __expf(gC - Gl[i]), a, b);
-        hh[i >> 3][i & 7] = a;
-        hl[i >> 3][i & 7] = b;
-      }
-#pragma unroll
-      for (int x = 0; x < 2; ++x) {
-        const int o = ch * C + 16 * hf + 8 * x;
-        *reinterpret_cast<bf16x8*>(sKGH + o) = gh[x];
-        *reinterpret_cast<bf16x8*>(sKGL + o) = gl[x];
-        *reinterpret_cast<bf16x8*>(sKHH + o) = hh[x];
-        *reinterpret_cast<bf16x8*>(sKHL + o) = hl[x];
-      }
-    }
-
     // ---- A = Diag(beta) (strictly lower part of R Q^T), three 16x16 tiles -----------
+    // fp32 MFMA (16x16x4): lane (q, r) feeds channel c = 16j + 4q + i to step (j, i), so
+    // the factors need no bf16 splitting.
     if (w < 3) {
       const int ti = w == 0 ? 0 : 1, si = w == 2 ? 1 : 0;
       const int rf = w == 0 ? 8 : (w == 1 ? 15 : 24);   // reference token of the tile
       const int tr = 16 * ti + r, sr = 16 * si + r;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+      for (int j = 0; j < 8; ++j) {
+        const int c0 = 16 * j + 4 * q;
+        const f32x4 gt = *reinterpret_cast<const f32x4*>(sG + tr * SG + c0);
+        const f32x4 gs = *reinterpret_cast<const f32x4*>(sG + sr * SG + c0);
+        const f32x4 gf = *reinterpret_cast<const f32x4*>(sG + rf * SG + c0);
+        const uint2 kt = *reinterpret_cast<const uint2*>(sK + tr * SK + c0);
+        const uint2 ks = *reinterpret_cast<const uint2*>(sK + sr * SK + c0);
+        const uint32_t ktw[2] = {kt.x, kt.y}, ksw[2] = {ks.x, ks.y};
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int c0 = 32 * kk + 8 * q;
-        bf16x8 rh, rl, qh, ql;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float gref = sG[rf * D + c0 + e];
-          __bf16 a, b;
-          split(bf2f(sK[tr * D + c0 + e]) * __expf(sG[tr * D + c0 + e] - gref), a, b);
-          rh[e] = a;
-          rl[e] = b;
-          split(bf2f(sK[sr * D + c0 + e]) * __expf(gref - sG[sr * D + c0 + e]), a, b);
-          qh[e] = a;
-          ql[e] = b;
+        for (int i = 0; i < 4; ++i) {
+          const float kte = __uint_as_float((i & 1) ? (ktw[i >> 1] & 0xFFFF0000u) : (ktw[i >> 1] << 16));
+          const float kse = __uint_as_float((i & 1) ? (ksw[i >> 1] & 0xFFFF0000u) : (ksw[i >> 1] << 16));
+          if (i & 1)
+            acc2 = mma32(kte * ex2(gt[i] - gf[i]), kse * ex2(gf[i] - gs[i]), acc2);
+          else
+            acc = mma32(kte * ex2(gt[i] - gf[i]), kse * ex2(gf[i] - gs[i]), acc);
         }
-        acc = mma3(rh, rl, qh, ql, acc);
       }
+      acc += acc2;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int t = 16 * ti + 4 * q + i;
-        const float val = (ti == si && sr >= t) ? 0.f : sBeta[t] * acc[i];
-        sA[t * C + sr] = val;
+        sA[t * C + sr] = (ti == si && sr >= t) ? 0.f : sBeta[t] * acc[i];
+      }
+    } else {
+      // meanwhile wave 3: K_H^T = (k exp(G_C - G))^T, rows = channels, split hi/lo
+#pragma unroll
+      for (int x = 0; x < 2; ++x) {
+        const int c = lane + 64 * x;
+        const float gC = sG[31 * SG + c];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          bf16x8 hh, hl;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int t = 8 * m + e;
+            __bf16 a, b;
+            split(bf2f(sK[t * SK + c]) * ex2(gC - sG[t * SG + c]), a, b);
+            hh[e] = a;
+            hl[e] = b;
+          }
+          *reinterpret_cast<bf16x8*>(sKHH + c * SV + 8 * m) = hh;
+          *reinterpret_cast<bf16x8*>(sKHL + c * SV + 8 * m) = hl;
+        }
       }
     }
     __syncthreads();
@@ -270,79 +304,70 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         sT[(base + t) * C + base + s] = acc;
       }
     }
-    __syncthreads();
-    {  // Y = A10 T00
-      const int t = tid >> 4, s = tid & 15;
-      float acc = 0.f;
+    // K_G = k exp(G), rows = tokens: this thread's two (token, 8-channel) units, whose
+    // keys it still holds from the load
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) acc = fmaf(sA[(16 + t) * C + rr], sT[rr * C + s], acc);
-      sY[t * 16 + s] = acc;
+    for (int u = 0; u < 2; ++u) {
+      const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
+      const uint32_t kw[4] = {kraw[u].x, kraw[u].y, kraw[u].z, kraw[u].w};
+      const f32x4 g0 = *reinterpret_cast<const f32x4*>(sG + t * SG + c8);
+      const f32x4 g1 = *reinterpret_cast<const f32x4*>(sG + t * SG + c8 + 4);
+      bf16x8 hh, hl;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float kv = t < nv ? __uint_as_float((e & 1) ? (kw[e >> 1] & 0xFFFF0000u) : (kw[e >> 1] << 16)) : 0.f;
+        __bf16 a, b;
+        split(kv * ex2(e < 4 ? g0[e & 3] : g1[e & 3]), a, b);
+        hh[e] = a;
+        hl[e] = b;
+      }
+      *reinterpret_cast<bf16x8*>(sKGH + t * SK + c8) = hh;
+      *reinterpret_cast<bf16x8*>(sKGL + t * SK + c8) = hl;
     }
+    // the next chunk's inputs load while this chunk finishes
+    if (t0 + C < W) fetch(t0 + C, min(C, W - t0 - C));
     __syncthreads();
-    {  // T10 = -T11 Y
-      const int t = tid >> 4, s = tid & 15;
-      float acc = 0.f;
+    // T' = T Diag(beta), split hi/lo.  Wave 1 forms the off-diagonal block
+    // T10 = -T11 (A10 T00) on fp32 MFMA, the product staying in registers between the
+    // two steps; the other waves write the diagonal blocks and the zero upper block.
+    if (w == 1) {
+      f32x4 y = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) acc = fmaf(sT[(16 + t) * C + 16 + rr], sY[rr * 16 + s], acc);
-      sT[(16 + t) * C + s] = -acc;
-    }
-    __syncthreads();
-    // T' = T Diag(beta), lower triangle only, split hi/lo
+      for (int i = 0; i < 4; ++i)
+        y = mma32(sA[(16 + r) * C + 4 * q + i], sT[(4 * q + i) * C + r], y);
+      f32x4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int e = tid + 256 * u;
-      const int t = e >> 5, s = e & 31;
-      const float val = s <= t ? sT[e] * sBeta[s] : 0.f;
-      __bf16 a, b;
-      split(val, a, b);
-      sTPH[e] = a;
-      sTPL[e] = b;
-    }
-    __syncthreads();
-
-    // ---- -(T' K_G) computed transposed: rows = channels of this wave's 32 ------------
+      for (int i = 0; i < 4; ++i) z = mma32(sT[(16 + r) * C + 16 + 4 * q + i], y[i], z);
+      const float br = sBeta[r];
 #pragma unroll
-    for (int mtw = 0; mtw < 2; ++mtw) {
-      const int cr = 32 * w + 16 * mtw + r;
-      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sKGH + cr * C + 8 * q);
-      const bf16x8 al = *reinterpret_cast<const bf16x8*>(sKGL + cr * C + 8 * q);
+      for (int i = 0; i < 4; ++i) {
+        const int t = 16 + 4 * q + i;
+        __bf16 a, b;
+        split(-z[i] * br, a, b);
+        sTPH[t * SP + r] = a;
+        sTPL[t * SP + r] = b;
+      }
+    } else {
+      const int lt = w == 0 ? tid : tid - 64;       // 0 .. 191
 #pragma unroll
-      for (int ntw = 0; ntw < 2; ++ntw) {
-        const int tr = 16 * ntw + r;
-        const bf16x8 bh = *reinterpret_cast<const bf16x8*>(sTPH + tr * C + 8 * q);
-        const bf16x8 bl = *reinterpret_cast<const bf16x8*>(sTPL + tr * C + 8 * q);
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        acc = mma3(ah, al, bh, bl, acc);
-        bf16x4 oh, ol;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
+      for (int u = 0; u < 4; ++u) {
+        // 768 entries outside block (1,0): rows 0..15 whole, rows 16..31 columns 16..31
+        const int e = lt + 192 * u;
+        const int t = e < 512 ? e >> 5 : 16 + ((e - 512) >> 4);
+        const int s = e < 512 ? e & 31 : 16 + ((e - 512) & 15);
+        {
+          const float val = s <= t ? sT[t * C + s] * sBeta[s] : 0.f;
           __bf16 a, b;
-          split(-acc[i], a, b);
-          oh[i] = a;
-          ol[i] = b;
+          split(val, a, b);
+          sTPH[t * SP + s] = a;
+          sTPL[t * SP + s] = b;
         }
-        const int o = tr * D + 32 * w + 16 * mtw + 4 * q;
-        *reinterpret_cast<bf16x4*>(sWNH + o) = oh;
-        *reinterpret_cast<bf16x4*>(sWNL + o) = ol;
       }
     }
     __syncthreads();
 
-    // ---- U = T'V - (T'K_G) S' on this wave's columns -----------------------------------
-    f32x4 U[2][2];
-#pragma unroll
-    for (int mu = 0; mu < 2; ++mu) {
-      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(sTPH + (16 * mu + r) * C + 8 * q);
-      const bf16x8 al = *reinterpret_cast<const bf16x8*>(sTPL + (16 * mu + r) * C + 8 * q);
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        const bf16x8 bv =
-            *reinterpret_cast<const bf16x8*>(sVT + (32 * w + 16 * nt + r) * C + 8 * q);
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        acc = mma(al, bv, acc);
-        U[mu][nt] = mma(ah, bv, acc);
-      }
-    }
+    // ---- X = K_G S' on this wave's columns (rows t, contraction over channels) -------
+    f32x4 X[2][2] = {};
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       bf16x8 sh[2], slo[2];
@@ -357,13 +382,46 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         }
 #pragma unroll
       for (int mu = 0; mu < 2; ++mu) {
-        const int o = (16 * mu + r) * D + 32 * kk + 4 * q;
-        const bf16x8 ah = cat(*reinterpret_cast<const bf16x4*>(sWNH + o),
-                              *reinterpret_cast<const bf16x4*>(sWNH + o + 16));
-        const bf16x8 al = cat(*reinterpret_cast<const bf16x4*>(sWNL + o),
-                              *reinterpret_cast<const bf16x4*>(sWNL + o + 16));
+        const int o = (16 * mu + r) * SK + 32 * kk + 4 * q;
+        const bf16x8 ah = cat(*reinterpret_cast<const bf16x4*>(sKGH + o),
+                              *reinterpret_cast<const bf16x4*>(sKGH + o + 16));
+        const bf16x8 al = cat(*reinterpret_cast<const bf16x4*>(sKGL + o),
+                              *reinterpret_cast<const bf16x4*>(sKGL + o + 16));
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) U[mu][nt] = mma3(ah, al, sh[nt], slo[nt], U[mu][nt]);
+        for (int nt = 0; nt < 2; ++nt) X[mu][nt] = mma3(ah, al, sh[nt], slo[nt], X[mu][nt]);
+      }
+    }
+
+    // ---- U = T' (V - X): the difference stays in registers as the B operand --------
+    f32x4 U[2][2];
+    {
+      bf16x8 yh[2], yl[2];
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        const int j = 32 * w + 16 * nt + r;
+#pragma unroll
+        for (int mu = 0; mu < 2; ++mu) {
+          const uint2 vv = *reinterpret_cast<const uint2*>(sVT + j * SV + 16 * mu + 4 * q);
+          const float vf[4] = {__uint_as_float(vv.x << 16), __uint_as_float(vv.x & 0xFFFF0000u),
+                               __uint_as_float(vv.y << 16), __uint_as_float(vv.y & 0xFFFF0000u)};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            __bf16 a, b;
+            split(vf[i] - X[mu][nt][i], a, b);
+            yh[nt][4 * mu + i] = a;
+            yl[nt][4 * mu + i] = b;
+          }
+        }
+      }
+#pragma unroll
+      for (int mu = 0; mu < 2; ++mu) {
+        const int o = (16 * mu + r) * SP + 4 * q;
+        const bf16x8 ah = cat(*reinterpret_cast<const bf16x4*>(sTPH + o),
+                              *reinterpret_cast<const bf16x4*>(sTPH + o + 16));
+        const bf16x8 al = cat(*reinterpret_cast<const bf16x4*>(sTPL + o),
+                              *reinterpret_cast<const bf16x4*>(sTPL + o + 16));
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) U[mu][nt] = mma3(ah, al, yh[nt], yl[nt], f32x4{0.f, 0.f, 0.f, 0.f});
       }
     }
 
@@ -381,16 +439,13 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
     for (int mt = 0; mt < 8; ++mt) {
       const f32x4 gam = *reinterpret_cast<const f32x4*>(sGam + 16 * mt + 4 * q);
-      const int o = (16 * mt + r) * C + 4 * q;
+      const int o = (16 * mt + r) * SV + 4 * q;
       const bf16x8 ah = cat(*reinterpret_cast<const bf16x4*>(sKHH + o),
                             *reinterpret_cast<const bf16x4*>(sKHH + o + 16));
       const bf16x8 al = cat(*reinterpret_cast<const bf16x4*>(sKHL + o),
                             *reinterpret_cast<const bf16x4*>(sKHL + o + 16));
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        f32x4 s = S[mt][nt] * gam;
-        S[mt][nt] = mma3(ah, al, uh[nt], ul[nt], s);
-      }
+      for (int nt = 0; nt < 2; ++nt) S[mt][nt] = mma3(ah, al, uh[nt], ul[nt], S[mt][nt] * gam);
     }
     __syncthreads();
   }
