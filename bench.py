@@ -32,7 +32,12 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 matrix peak
 FP32_VALU_PEAK_TFLOPS = 78.6    # 256 CU x 64 FMA lanes/clk x 2 FLOP x 2.4 GHz (no packed FP32)
+# Chunked WY form at 32-token chunks, dk = dv = 128, per head-token: the three 16x16
+# A tiles (3*16*16*128 MAC), K_G S (32*128*128), T'(V - K_G S) (32*32*128)
+# and K_H^T U (128*32*128), per 32 tokens, 2 FLOP per MAC.
+WY_FLOP_PER_HEAD_TOKEN = 2.0 * (3 * 16 * 16 * 128 + 32 * 128 * 128 + 32 * 32 * 128 + 128 * 32 * 128) / 32
 METRIC = "pack/restore GB/s + suffix-refresh tokens/s (KDA 32h x 128x128, W=1024)"
 
 
@@ -52,7 +57,8 @@ def parse():
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("pack_restore.hip", "refresh.hip", "launch_common.h"):
+    for f in ("pack_restore.hip", "refresh.hip", "refresh_wy.hip", "refresh_kernels.h",
+              "launch_common.h"):
         with open(os.path.join(ROOT, "paper_2608_30386_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -193,7 +199,7 @@ def bench_headline(torch, args):
     # writes the omitted rows
     per_head = (2 * W * sh.dk + 2 * W * dv + 4 * W * sh.dk + 4 * W + 4 * sh.dk * dv)
     bytes_refresh = n_req * (heads_refreshed * per_head + int(omitted.sum()) * dv * 4)
-    flops_refresh = 5.0 * sh.dk * dv * W * n_req * heads_refreshed   # decay, read-out, write
+    flops_refresh = WY_FLOP_PER_HEAD_TOKEN * W * n_req * heads_refreshed
 
     t = {n: timer.mean_ms(n) for n in ("pack", "restore", "refresh")}
     kernels = {
@@ -207,7 +213,7 @@ def bench_headline(torch, args):
                     "TFLOPs": flops_refresh / t["refresh"] / 1e9, "bytes": bytes_refresh,
                     "flops": flops_refresh, "heads": n_req * heads_refreshed},
     }
-    achieved = flops_refresh / (t["refresh"] / 1e3) / 1e12
+    achieved = bytes_refresh / t["refresh"] / 1e6          # GB/s
     traffic = measured_traffic("refresh")
     out = {
         "metric": METRIC,
@@ -224,10 +230,12 @@ def bench_headline(torch, args):
             "n_checkpoints": n_ckpt, "n_requests": n_req, "W": W, "rows_kept": R,
             "inputs": "k,v bf16; g,beta fp32; state fp32",
         },
-        "roofline": {"bound": "alu", "achieved": achieved, "peak": FP32_VALU_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / FP32_VALU_PEAK_TFLOPS,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": traffic, "kernel": "refresh",
-                     "work_per_launch": f"{flops_refresh:.4g} FLOP = 5*dk*dv per head-token"},
+                     "work_per_launch": f"{bytes_refresh} B = per refreshed head: k, v (bf16), g, "
+                                        "beta (fp32), restored state read, omitted rows written",
+                     "mfma_frac": flops_refresh / (t["refresh"] / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS},
         "kernels": kernels,
         "pack_restore_GBps": (bytes_pack + bytes_restore) / (t["pack"] + t["restore"]) / 1e6,
         "plan_host_ms": plan_s * 1e3,
@@ -244,7 +252,7 @@ def cpu_baseline_headline(wl, plan, states_np, inp, W, n_req):
     from oracle import pack as OK
     from oracle import recurrence as OR
 
-    n_s, req_s = 8, 2                         # 8 of 64 checkpoints, 2 of 16 requests
+    n_s, req_s = wl.n_ckpt, n_req // 2        # all checkpoints, half the requests
     R = int(plan["n_rows"])
     words = states_np.reshape(states_np.shape[0], -1, wl.dv).view(np.uint32)
     with threadpool_limits(1):
@@ -266,9 +274,9 @@ def cpu_baseline_headline(wl, plan, states_np, inp, W, n_req):
     scale_ck = wl.n_ckpt / n_s
     step_s = (t_pack + t_restore) * scale_ck + t_ref * n_req / req_s
     return {"value": n_req * W / step_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"pack+restore {n_s} of {wl.n_ckpt} checkpoints, refresh {req_s} of "
-                      f"{n_req} requests (all 32 heads, W={W}, fp64 per-token form); "
-                      "scaled linearly to the full step",
+            "sample": f"pack+restore all {n_s} checkpoints, refresh {req_s} of {n_req} requests "
+                      f"x 32 heads at W={W} (fp64 per-token form, vectorised over heads); the "
+                      "refresh time is scaled to all requests",
             "sample_seconds": t_pack + t_restore + t_ref,
             "host_cpus": os.cpu_count()}
 

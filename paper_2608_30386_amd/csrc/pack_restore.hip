@@ -15,6 +15,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "dasc.h"
@@ -54,21 +55,30 @@ __device__ inline int64_t slice_row(int64_t j, int64_t slice_rows, int64_t n_row
 // Rows per block: enough 128-bit vectors for every thread to move kUnroll of them.
 inline int rows_per_block(int vpr) { return vpr >= kVecPerBlock ? 1 : kVecPerBlock / vpr; }
 
+// A block owns a tile of rows of one rank slice of one checkpoint, so the slice of a
+// packed row is known per block and the destination needs no per-row division.
 template <int VPR_LOG2>
 __global__ __launch_bounds__(kThreads) void pack_kernel(
     const f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
     const int32_t* __restrict__ src_slot, const int32_t* __restrict__ unit_row, int64_t n_rows,
     f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ dst_slot,
-    int64_t slice_rows, int blocks_per_ckpt, int rpb, int vpr_rt) {
+    int64_t slice_rows, int n_ranks, int blocks_per_slice, int rpb, int vpr_rt) {
   using G = RowGeom<VPR_LOG2>;
   const int vpr = G::vpr(vpr_rt);
-  const int i = blockIdx.x / blocks_per_ckpt;
-  const int rb = blockIdx.x - i * blocks_per_ckpt;
+  const int per_ckpt = n_ranks * blocks_per_slice;
+  const int i = blockIdx.x / per_ckpt;
+  const int rem = blockIdx.x - i * per_ckpt;
+  const int rk = rem / blocks_per_slice;
+  const int rb = rem - rk * blocks_per_slice;
   const int64_t s = src_slot[i];
   const int64_t d = dst_slot[i];
   if (s < 0 || s >= n_pool || d < 0 || d >= n_ckpt_slots) return;
   const f32x4* src = states + s * rows_state * vpr;
-  const int64_t row0 = int64_t(rb) * rpb;
+  const int64_t slice0 = int64_t(rk) * slice_rows;                 // first packed row of the slice
+  const int64_t slice_end = min(slice0 + slice_rows, n_rows);
+  const int64_t row0 = slice0 + int64_t(rb) * rpb;
+  // offset of packed row 0 of this slice (may be negative; every row used is >= slice0)
+  const int64_t dbase = ((int64_t(rk) * n_ckpt_slots + d) * slice_rows - slice0) * vpr;
   const int n_vec = rpb * vpr;
 
   for (int base = 0; base < n_vec; base += kVecPerBlock) {
@@ -79,18 +89,18 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(
       const int v = base + u * kThreads + threadIdx.x;
       const int64_t j = row0 + G::row_of(v, vpr_rt);
       dst_off[u] = -1;
-      if (v < n_vec && j < n_rows) {
+      if (v < n_vec && j < slice_end) {
         const int64_t dense = unit_row[j];
         if (dense >= 0 && dense < rows_state) {
           const int c = G::col_of(v, vpr_rt);
           val[u] = __builtin_nontemporal_load(src + dense * vpr + c);
-          dst_off[u] = slice_row(j, slice_rows, n_rows, n_ckpt_slots, d) * vpr + c;
+          dst_off[u] = j * vpr + c;
         }
       }
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u)
-      if (dst_off[u] >= 0) __builtin_nontemporal_store(val[u], ckpt + dst_off[u]);
+      if (dst_off[u] >= 0) __builtin_nontemporal_store(val[u], ckpt + (dbase + dst_off[u]));
   }
 }
 
@@ -180,14 +190,16 @@ extern "C" int dasc_pack(const dasc_shape* shape, const float* states, int64_t n
   if (!dasc::aligned16(states) || !dasc::aligned16(ckpt)) return DASC_E_INVAL;
   const int vpr = shape->dv / 4;
   const int rpb = rows_per_block(vpr);
-  const int64_t bpc = (n_rows + rpb - 1) / rpb;
-  if (bpc * n > INT32_MAX) return DASC_E_INVAL;
+  // blocks per rank slice: a slice holds at most min(slice_rows, n_rows) packed rows
+  const int64_t bps = (std::min<int64_t>(slice_rows, n_rows) + rpb - 1) / rpb;
+  const int64_t blocks = bps * n_ranks * n;
+  if (blocks > INT32_MAX) return DASC_E_INVAL;
   (void)hipGetLastError();
-  DASC_LAUNCH_BY_VPR(pack_kernel, vpr_log2(vpr), dim3(unsigned(bpc * n)),
+  DASC_LAUNCH_BY_VPR(pack_kernel, vpr_log2(vpr), dim3(unsigned(blocks)),
                      reinterpret_cast<hipStream_t>(stream),
                      reinterpret_cast<const f32x4*>(states), n_pool, dasc::rows_per_state(shape),
                      src_slot, unit_row, n_rows, reinterpret_cast<f32x4*>(ckpt), n_ckpt_slots,
-                     dst_slot, slice_rows, int(bpc), rpb, vpr);
+                     dst_slot, slice_rows, int(n_ranks), int(bps), rpb, vpr);
   return dasc::launch_status();
 }
 
