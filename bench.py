@@ -57,14 +57,14 @@ def parse():
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("pack_restore.hip", "refresh.hip", "refresh_wy.hip", "refresh_kernels.h",
-              "launch_common.h"):
+    for f in ("pack_restore.hip", "quant.hip", "refresh.hip", "refresh_wy.hip",
+              "refresh_kernels.h", "launch_common.h"):
         with open(os.path.join(ROOT, "paper_2608_30386_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str):
+def measured_traffic(key: str):
     """HBM bytes per launch from the committed counter summary, if it matches this source."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
@@ -73,7 +73,7 @@ def measured_traffic(kernel: str):
         t = json.load(fh)
     if t.get("source_hash") != kernel_source_hash():
         return None
-    return t.get("kernels", {}).get(kernel)
+    return t.get("kernels", {}).get(key)
 
 
 class KernelTimer:
@@ -214,7 +214,7 @@ def bench_headline(torch, args):
                     "flops": flops_refresh, "heads": n_req * heads_refreshed},
     }
     achieved = bytes_refresh / t["refresh"] / 1e6          # GB/s
-    traffic = measured_traffic("refresh")
+    traffic = measured_traffic("kimi_headline/refresh")
     out = {
         "metric": METRIC,
         "value": n_req * W / (ms_step / 1e3),
@@ -319,6 +319,24 @@ def bench_pack_restore_only(torch, args, name):
     dom = "restore" if t["restore"] >= t["pack"] else "pack"
     dom_bytes = br if dom == "restore" else bp
     ach = dom_bytes / t[dom] / 1e6
+
+    # INT8 checkpoints (App. E.1) on the same states, flat layout, timed separately
+    del ckpt
+    q = torch.empty((n, R, dv), dtype=torch.int8, device="cuda")
+    s = torch.empty((n, R), dtype=torch.float32, device="cuda")
+    for _ in range(args.warmup):
+        D.dasc_pack_q8(sh, states, ids, unit_row, q, s, ids)
+        D.dasc_restore_q8(sh, q, s, ids, inv_row, active, ids, n_rows=R)
+    torch.cuda.synchronize()
+    timer.spans.clear()
+    for _ in range(args.steps):
+        timer.run("pack_q8", lambda: D.dasc_pack_q8(sh, states, ids, unit_row, q, s, ids))
+        timer.run("restore_q8", lambda: D.dasc_restore_q8(sh, q, s, ids, inv_row, active, ids,
+                                                          n_rows=R))
+    torch.cuda.synchronize()
+    tq = {k_: timer.mean_ms(k_) for k_ in ("pack_q8", "restore_q8")}
+    bpq = R * n * (dv * 4 + dv + 4)               # read fp32 rows, write int8 rows + scales
+    brq = n * (R * (dv + 4) + rows * dv * 4)      # read int8 rows + scales, write fp32 states
     return {
         "metric": "pack+restore GB/s (full-model KDA checkpoint set)", "value": gbps, "unit": "GB/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
@@ -327,9 +345,13 @@ def bench_pack_restore_only(torch, args, name):
         "config": {"workload": f"{wl.n_layers} KDA layers x 32h x 128x128 fp32, {n} checkpoints, "
                                f"R={R} of {rows} rows kept, T={T} rank slices"},
         "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": ach / HBM_PEAK_GBPS, "traffic": measured_traffic(dom), "kernel": dom},
-        "kernels": {k_: {"ms": t[k_], "GBps": b / t[k_] / 1e6, "hbm_frac": b / t[k_] / 1e6 / HBM_PEAK_GBPS,
-                         "bytes": b} for k_, b in (("pack", bp), ("restore", br))},
+                     "frac": ach / HBM_PEAK_GBPS, "traffic": measured_traffic(f"{name}/{dom}"),
+                     "kernel": dom},
+        "kernels": {k_: {"ms": tt[k_], "GBps": b / tt[k_] / 1e6,
+                         "hbm_frac": b / tt[k_] / 1e6 / HBM_PEAK_GBPS, "bytes": b}
+                    for tt, k_, b in ((t, "pack", bp), (t, "restore", br),
+                                      (tq, "pack_q8", bpq), (tq, "restore_q8", brq))},
+        "q8_checkpoint_bytes": R * (dv + 4), "fp32_checkpoint_bytes": R * dv * 4,
         "plan_host_ms": plan_s * 1e3,
     }
 

@@ -189,6 +189,34 @@ int dasc_restore(const dasc_shape *shape,
                  float *states, int64_t n_pool, const int32_t *dst_slot,
                  int32_t n, dasc_stream_t stream);
 
+/* ---- INT8 checkpoints (App. E.1, Eq. 10) ---------------------------------- */
+
+/* Pack with symmetric INT8 quantisation.  One scale per (layer, head, key channel),
+ * shared over dv -- one scale per state row here: for packed row j of checkpoint i,
+ *     a = max_v |x_v|,  s = max(a, 1e-8) / 127,  q_v = clip(rne(x_v / s), -127, 127),
+ * with x = states[src_slot[i]][unit_row[j]][:], computed in FP32 with correctly rounded
+ * divisions; q[dst_slot[i]][j][:] = q_v (int8), scale[dst_slot[i]][j] = s (FP32).
+ *   states: device fp32 pool [n_pool, L*H*dk, dv], 16-byte aligned.
+ *   q: device int8 [n_ckpt_slots, n_rows, dv], 4-byte aligned.
+ *   scale: device fp32 [n_ckpt_slots, n_rows].
+ *   unit_row: device int32 [n_rows]; src_slot, dst_slot: device int32 [n].
+ * Flat layout only (no rank slices).  States must be finite.
+ * Errors: as dasc_pack; DASC_E_UNSUPPORTED unless dv is a power of two in [4, 1024]. */
+int dasc_pack_q8(const dasc_shape *shape, const float *states, int64_t n_pool,
+                 const int32_t *src_slot, const int32_t *unit_row, int64_t n_rows,
+                 int8_t *q, float *scale, int64_t n_ckpt_slots, const int32_t *dst_slot,
+                 int32_t n, dasc_stream_t stream);
+
+/* Restore from INT8 checkpoints: dequantise once into fresh FP32 active states,
+ *     states[dst_slot[i]][d][:] = (0 <= p < n_rows) ? q[src_slot[i]][p][:] * scale[src_slot[i]][p]
+ *                                                   : +0.0,    p = inv_row[d],
+ * for every dense row d (the product is one FP32 multiply per element).
+ * Arguments as dasc_pack_q8 / dasc_restore.  Errors: as dasc_pack_q8. */
+int dasc_restore_q8(const dasc_shape *shape, const int8_t *q, const float *scale,
+                    int64_t n_ckpt_slots, const int32_t *src_slot, int64_t n_rows,
+                    const int32_t *inv_row, float *states, int64_t n_pool,
+                    const int32_t *dst_slot, int32_t n, dasc_stream_t stream);
+
 /* ---- Load with refresh: bounded-suffix replay (Sec. 4.2 DASC-WR, Eq. 1) --- */
 
 /* Device workspace dasc_refresh needs for n_req requests and window W (may be 0).

@@ -28,7 +28,8 @@ DASC_INIT_ZERO = 1
 
 EXPORTED = (
     "dasc_static_log_decay", "dasc_plan", "dasc_matched_slots", "dasc_strerror",
-    "dasc_pack", "dasc_restore", "dasc_refresh_workspace_bytes", "dasc_refresh",
+    "dasc_pack", "dasc_restore", "dasc_pack_q8", "dasc_restore_q8",
+    "dasc_refresh_workspace_bytes", "dasc_refresh",
 )
 
 
@@ -69,7 +70,7 @@ def _hip_runtimes() -> set:
 def _load() -> C.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(
-            f"{LIB_PATH} is missing: build it with `python -m paper_2608_30386_amd.build` "
+            f"{LIB_PATH} is missing: build it with `python paper_2608_30386_amd/build.py` "
             "(there is no non-HIP fallback)")
     # torch supplies device memory and streams, so the library must run on torch's HIP
     # runtime: load torch first, and libdasc.so then binds to the libamdhip64 already
@@ -88,6 +89,8 @@ def _load() -> C.CDLL:
         "dasc_matched_slots": [I64, I64, C.POINTER(C.c_int64)],
         "dasc_pack": [C.POINTER(Shape), P, I64, P, P, I64, P, I64, P, I32, I64, I32, P],
         "dasc_restore": [C.POINTER(Shape), P, I64, P, I32, I64, I64, P, P, I64, P, I32, P],
+        "dasc_pack_q8": [C.POINTER(Shape), P, I64, P, P, I64, P, P, I64, P, I32, P],
+        "dasc_restore_q8": [C.POINTER(Shape), P, P, I64, P, I64, P, P, I64, P, I32, P],
         "dasc_refresh_workspace_bytes": [C.POINTER(Shape), I32, I32, C.POINTER(C.c_size_t)],
         "dasc_refresh": [C.POINTER(Shape), I32, P, P, I64, P, P, P, P, P, I32, I32, I32, P, SZ, P],
     }

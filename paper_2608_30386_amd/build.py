@@ -1,6 +1,6 @@
 """Build libdasc.so in-tree: HIP kernels for gfx950 plus the host planner.
 
-    python -m paper_2608_30386_amd.build
+    python paper_2608_30386_amd/build.py
 
 HIP sources are compiled by hipcc for gfx950 only; packed-FP32 instructions are
 disabled for all device code.  The planner is plain host C++ compiled by g++
@@ -21,7 +21,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdasc.so")
 
-HIP_SOURCES = ["pack_restore.hip", "refresh.hip", "refresh_wy.hip"]
+HIP_SOURCES = ["pack_restore.hip", "quant.hip", "refresh.hip", "refresh_wy.hip"]
 HOST_SOURCES = ["plan.cpp"]
 ARCH = "gfx950"
 

@@ -175,6 +175,40 @@ def dasc_restore(shape: Shape, ckpt, src_slot, inv_row, states, dst_slot, n_rows
         _stream(stream)), "dasc_restore")
 
 
+def dasc_pack_q8(shape: Shape, states, src_slot, unit_row, q, scale, dst_slot, stream=None) -> None:
+    """INT8 pack: q [n_slots, R, dv] int8, scale [n_slots, R] float32 (see dasc.h)."""
+    import torch
+
+    n_rows = unit_row.numel()
+    n_slots = q.shape[0]
+    _need(states, states.shape[0] * shape.rows * shape.dv, "states")
+    _need(q, n_slots * n_rows * shape.dv, "q")
+    _need(scale, n_slots * n_rows, "scale")
+    _need(dst_slot, src_slot.numel(), "dst_slot")
+    _check(LIB.dasc_pack_q8(
+        C.byref(shape.c()), _dev(states, torch.float32, "states"), states.shape[0],
+        _dev(src_slot, torch.int32, "src_slot"), _dev(unit_row, torch.int32, "unit_row"), n_rows,
+        _dev(q, torch.int8, "q"), _dev(scale, torch.float32, "scale"), n_slots,
+        _dev(dst_slot, torch.int32, "dst_slot"), src_slot.numel(), _stream(stream)), "dasc_pack_q8")
+
+
+def dasc_restore_q8(shape: Shape, q, scale, src_slot, inv_row, states, dst_slot, n_rows: int,
+                    stream=None) -> None:
+    import torch
+
+    n_slots = q.shape[0]
+    _need(states, states.shape[0] * shape.rows * shape.dv, "states")
+    _need(q, n_slots * n_rows * shape.dv, "q")
+    _need(scale, n_slots * n_rows, "scale")
+    _need(inv_row, shape.rows, "inv_row")
+    _need(dst_slot, src_slot.numel(), "dst_slot")
+    _check(LIB.dasc_restore_q8(
+        C.byref(shape.c()), _dev(q, torch.int8, "q"), _dev(scale, torch.float32, "scale"), n_slots,
+        _dev(src_slot, torch.int32, "src_slot"), n_rows, _dev(inv_row, torch.int32, "inv_row"),
+        _dev(states, torch.float32, "states"), states.shape[0],
+        _dev(dst_slot, torch.int32, "dst_slot"), src_slot.numel(), _stream(stream)), "dasc_restore_q8")
+
+
 def dasc_refresh_workspace_bytes(shape: Shape, n_req: int, W: int) -> int:
     out = C.c_size_t()
     _check(LIB.dasc_refresh_workspace_bytes(C.byref(shape.c()), n_req, W, C.byref(out)),
