@@ -54,6 +54,10 @@ extern "C" {
 #define DASC_E_HIP         -4  /* the HIP runtime reported an error at launch    */
 #define DASC_E_UNSUPPORTED -5  /* valid request with no kernel built for it      */
 
+/* Longest replay window dasc_refresh accepts (tokens): keeps every per-head input
+ * stream of a dk = 128 head within 1 GiB. */
+#define DASC_MAX_WINDOW (1 << 21)
+
 /* ---- enumerations -------------------------------------------------------- */
 #define DASC_ARCH_KDA 0  /* channel-wise decay: unit = one (head, key channel) row */
 #define DASC_ARCH_GDN 1  /* head-wise decay:    unit = one whole head              */
@@ -243,7 +247,7 @@ int dasc_refresh_workspace_bytes(const dasc_shape *shape, int32_t n_req, int32_t
  *   workspace: device, at least dasc_refresh_workspace_bytes (may be NULL if that is 0).
  * Arithmetic is fp32 with bf16 inputs widened exactly.
  * Errors: DASC_E_INVAL (NULL pointer, misalignment, layer out of [0, L), n_req < 1,
- * W < 1, bad init_mode, n_pool < 1), DASC_E_SHAPE (bad shape), DASC_E_WORKSPACE,
+ * W < 1 or W > DASC_MAX_WINDOW, bad init_mode, n_pool < 1), DASC_E_SHAPE (bad shape), DASC_E_WORKSPACE,
  * DASC_E_UNSUPPORTED (dk not in {16, 32, 64, 128} or dv > 256), DASC_E_HIP. */
 int dasc_refresh(const dasc_shape *shape, int32_t layer, const int32_t *inv_row,
                  float *states, int64_t n_pool, const int32_t *slot,

@@ -17,6 +17,7 @@ DASC_E_SHAPE = -2
 DASC_E_WORKSPACE = -3
 DASC_E_HIP = -4
 DASC_E_UNSUPPORTED = -5
+DASC_MAX_WINDOW = 1 << 21
 
 DASC_ARCH_KDA = 0
 DASC_ARCH_GDN = 1

@@ -131,7 +131,8 @@ extern "C" int dasc_refresh(const dasc_shape* shape, int32_t layer, const int32_
                             void* workspace, size_t workspace_bytes, dasc_stream_t stream) {
   if (!shape) return DASC_E_INVAL;
   if (!dasc::valid_shape(shape) || shape->dv % 4 != 0) return DASC_E_SHAPE;
-  if (layer < 0 || layer >= shape->n_layers || n_req < 1 || W < 1 || n_pool < 1)
+  if (layer < 0 || layer >= shape->n_layers || n_req < 1 || W < 1 || W > DASC_MAX_WINDOW ||
+      n_pool < 1)
     return DASC_E_INVAL;
   if (init_mode != DASC_INIT_RESTORED && init_mode != DASC_INIT_ZERO) return DASC_E_INVAL;
   if (!inv_row || !states || !slot || !k || !v || !g || !beta) return DASC_E_INVAL;

@@ -49,7 +49,9 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int C = 32;       // tokens per chunk
 constexpr int D = 128;      // dk = dv
@@ -82,11 +84,36 @@ static_assert(C * C * 4 + 2 * C * SP * 2 <= C * SK * 2, "T and T' must fit in th
 static_assert(LDS_BYTES <= 81920, "two blocks per CU");
 
 __device__ inline float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
+
+// Raw buffer resource over exactly `bytes` bytes: a load whose total offset (vector +
+// scalar + immediate) reaches past the end returns zero instead of touching memory.
+// Tokens past the window therefore arrive as k = v = 0, g = 0, beta = 0, which are
+// identity steps of the recurrence, and no load needs a clamp or a mask.
+__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
+}
+__device__ inline float ldf(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
 __device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ inline void split(float x, __bf16& hi, __bf16& lo) {
   hi = static_cast<__bf16>(x);
   lo = static_cast<__bf16>(x - static_cast<float>(hi));
+}
+
+// Eight values split at once: two values per packed conversion (3 VALU per value).
+__device__ inline void split8(const float* x, bf16x8& hi, bf16x8& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const uint32_t hw = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x[2 * p], x[2 * p + 1]}, bf16x2));
+    const float r0 = __uint_as_float(hw << 16), r1 = __uint_as_float(hw & 0xFFFF0000u);
+    h[p] = hw;
+    l[p] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x[2 * p] - r0, x[2 * p + 1] - r1}, bf16x2));
+  }
+  hi = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
+  lo = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
 }
 
 __device__ inline f32x4 mma(bf16x8 a, bf16x8 b, f32x4 c) {
@@ -158,68 +185,61 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   const uint16_t* vp = v + (int64_t(n) * H + h) * W * D;
   const float* gp = PER_CHANNEL ? g + (int64_t(n) * H + h) * W * D : g + (int64_t(n) * H + h) * W;
   const float* bp = beta + (int64_t(n) * H + h) * W;
+  const __amdgpu_buffer_rsrc_t rk = rsrc(kp, W * D * 2), rv = rsrc(vp, W * D * 2);
+  const __amdgpu_buffer_rsrc_t rg = rsrc(gp, PER_CHANNEL ? W * D * 4 : W * 4), rb = rsrc(bp, W * 4);
 
   const int ch = tid & (D - 1);   // channel (or value column) owned in the load phases
   const int hf = tid >> 7;        // which 16-token half of the chunk
 
-  // Gates, keys and beta of one chunk as this thread loads them.  Loads are
-  // unconditional (index clamped to the last valid token, value masked when consumed)
-  // so that all of them are in flight together; the next chunk's are issued one chunk
-  // ahead.  Values are loaded at the top of each chunk (registers are the limit).
+  // Gates, keys and beta of one chunk as this thread loads them; the next chunk's are
+  // issued one chunk ahead.  Values are loaded at the top of each chunk (registers
+  // are the limit).
   float graw[16];
   uint4 kraw[2];
   float braw;
-  auto fetch = [&](int c0, int nvalid) {
+  auto fetch = [&](int c0) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int tc = c0 + min(16 * hf + i, nvalid - 1);
-      graw[i] = PER_CHANNEL ? gp[int64_t(tc) * D + ch] : gp[tc];
-    }
+    for (int i = 0; i < 16; ++i)
+      graw[i] = PER_CHANNEL ? ldf(rg, ((16 * hf + i) * D + ch) * 4, c0 * D * 4)
+                            : ldf(rg, (16 * hf + i) * 4, c0 * 4);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
-      kraw[u] = *reinterpret_cast<const uint4*>(kp + int64_t(c0 + min(t, nvalid - 1)) * D + c8);
+      kraw[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, (t * D + c8) * 2, c0 * D * 2, 0));
     }
-    braw = bp[c0 + min(tid & (C - 1), nvalid - 1)];
+    braw = ldf(rb, (tid & (C - 1)) * 4, c0 * 4);
   };
-  fetch(0, min(C, W));
+  fetch(0);
 
   for (int t0 = 0; t0 < W; t0 += C) {
-    const int nv = min(C, W - t0);  // valid tokens; the rest are zero (identity) tokens
-
     // ---- values of this chunk (issued first), then the prefetched gates, keys, beta ---
     uint16_t vraw[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) vraw[i] = vp[int64_t(t0 + min(16 * hf + i, nv - 1)) * D + ch];
+    for (int i = 0; i < 16; ++i)
+      vraw[i] = __builtin_amdgcn_raw_buffer_load_b16(rv, ((16 * hf + i) * D + ch) * 2, t0 * D * 2, 0);
     float Gl[16];
     {
       float run = 0.f;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float gv = 16 * hf + i < nv ? graw[i] : 0.f;
-        run += fmaxf(gv, kGateFloor) * kLog2e;
+        run += fmaxf(graw[i], kGateFloor) * kLog2e;
         Gl[i] = run;
       }
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
-      *reinterpret_cast<uint4*>(sK + t * SK + c8) = t < nv ? kraw[u] : make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4*>(sK + t * SK + c8) = kraw[u];
     }
     {  // value column ch, tokens 16hf .. 16hf+15 -> one transposed row segment
       uint32_t pk[8];
 #pragma unroll
-      for (int i = 0; i < 16; i += 2) {
-        const int t = 16 * hf + i;
-        const uint32_t a = t < nv ? vraw[i] : 0u;
-        const uint32_t b = t + 1 < nv ? vraw[i + 1] : 0u;
-        pk[i >> 1] = a | (b << 16);
-      }
+      for (int i = 0; i < 16; i += 2) pk[i >> 1] = uint32_t(vraw[i]) | (uint32_t(vraw[i + 1]) << 16);
       uint4* dst = reinterpret_cast<uint4*>(sVT + ch * SV + 16 * hf);
       dst[0] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
       dst[1] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
     }
-    if (tid < C) sBeta[tid] = tid < nv ? braw : 0.f;
+    if (tid < C) sBeta[tid] = braw;
 #pragma unroll
     for (int i = 0; i < 16; ++i) sG[(16 * hf + i) * SG + ch] = Gl[i];
     __syncthreads();
@@ -275,15 +295,14 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         const float gC = sG[31 * SG + c];
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
-          bf16x8 hh, hl;
+          float x[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int t = 8 * m + e;
-            __bf16 a, b;
-            split(bf2f(sK[t * SK + c]) * ex2(gC - sG[t * SG + c]), a, b);
-            hh[e] = a;
-            hl[e] = b;
+            x[e] = bf2f(sK[t * SK + c]) * ex2(gC - sG[t * SG + c]);
           }
+          bf16x8 hh, hl;
+          split8(x, hh, hl);
           *reinterpret_cast<bf16x8*>(sKHH + c * SV + 8 * m) = hh;
           *reinterpret_cast<bf16x8*>(sKHL + c * SV + 8 * m) = hl;
         }
@@ -312,20 +331,19 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       const uint32_t kw[4] = {kraw[u].x, kraw[u].y, kraw[u].z, kraw[u].w};
       const f32x4 g0 = *reinterpret_cast<const f32x4*>(sG + t * SG + c8);
       const f32x4 g1 = *reinterpret_cast<const f32x4*>(sG + t * SG + c8 + 4);
-      bf16x8 hh, hl;
+      float x[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float kv = t < nv ? __uint_as_float((e & 1) ? (kw[e >> 1] & 0xFFFF0000u) : (kw[e >> 1] << 16)) : 0.f;
-        __bf16 a, b;
-        split(kv * ex2(e < 4 ? g0[e & 3] : g1[e & 3]), a, b);
-        hh[e] = a;
-        hl[e] = b;
+        const float kv = __uint_as_float((e & 1) ? (kw[e >> 1] & 0xFFFF0000u) : (kw[e >> 1] << 16));
+        x[e] = kv * ex2(e < 4 ? g0[e & 3] : g1[e & 3]);
       }
+      bf16x8 hh, hl;
+      split8(x, hh, hl);
       *reinterpret_cast<bf16x8*>(sKGH + t * SK + c8) = hh;
       *reinterpret_cast<bf16x8*>(sKGL + t * SK + c8) = hl;
     }
     // the next chunk's inputs load while this chunk finishes
-    if (t0 + C < W) fetch(t0 + C, min(C, W - t0 - C));
+    fetch(t0 + C);   // past the window this reads zeros
     __syncthreads();
     // T' = T Diag(beta), split hi/lo.  Wave 1 forms the off-diagonal block
     // T10 = -T11 (A10 T00) on fp32 MFMA, the product staying in registers between the
@@ -372,14 +390,12 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     for (int kk = 0; kk < 4; ++kk) {
       bf16x8 sh[2], slo[2];
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
+      for (int nt = 0; nt < 2; ++nt) {
+        float x[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          __bf16 a, b;
-          split(S[2 * kk + (e >> 2)][nt][e & 3], a, b);
-          sh[nt][e] = a;
-          slo[nt][e] = b;
-        }
+        for (int e = 0; e < 8; ++e) x[e] = S[2 * kk + (e >> 2)][nt][e & 3];
+        split8(x, sh[nt], slo[nt]);
+      }
 #pragma unroll
       for (int mu = 0; mu < 2; ++mu) {
         const int o = (16 * mu + r) * SK + 32 * kk + 4 * q;
@@ -399,19 +415,16 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
         const int j = 32 * w + 16 * nt + r;
+        float x[8];
 #pragma unroll
         for (int mu = 0; mu < 2; ++mu) {
           const uint2 vv = *reinterpret_cast<const uint2*>(sVT + j * SV + 16 * mu + 4 * q);
           const float vf[4] = {__uint_as_float(vv.x << 16), __uint_as_float(vv.x & 0xFFFF0000u),
                                __uint_as_float(vv.y << 16), __uint_as_float(vv.y & 0xFFFF0000u)};
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            __bf16 a, b;
-            split(vf[i] - X[mu][nt][i], a, b);
-            yh[nt][4 * mu + i] = a;
-            yl[nt][4 * mu + i] = b;
-          }
+          for (int i = 0; i < 4; ++i) x[4 * mu + i] = vf[i] - X[mu][nt][i];
         }
+        split8(x, yh[nt], yl[nt]);
       }
 #pragma unroll
       for (int mu = 0; mu < 2; ++mu) {
@@ -428,14 +441,12 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     // ---- S' <- Diag(exp(G_C)) S' + K_H^T U ----------------------------------------------
     bf16x8 uh[2], ul[2];
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
+    for (int nt = 0; nt < 2; ++nt) {
+      float x[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        __bf16 a, b;
-        split(U[e >> 2][nt][e & 3], a, b);
-        uh[nt][e] = a;
-        ul[nt][e] = b;
-      }
+      for (int e = 0; e < 8; ++e) x[e] = U[e >> 2][nt][e & 3];
+      split8(x, uh[nt], ul[nt]);
+    }
 #pragma unroll
     for (int mt = 0; mt < 8; ++mt) {
       const f32x4 gam = *reinterpret_cast<const f32x4*>(sGam + 16 * mt + 4 * q);

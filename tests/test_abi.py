@@ -91,6 +91,7 @@ def test_refresh_argument_errors():
     assert refresh(kda(dv=6)) == E.DASC_E_SHAPE
     assert refresh(kda(), W=0) == E.DASC_E_INVAL
     assert refresh(kda(), W=-3) == E.DASC_E_INVAL
+    assert refresh(kda(), W=E.DASC_MAX_WINDOW + 1) == E.DASC_E_INVAL
     assert refresh(kda(), layer=2) == E.DASC_E_INVAL
     assert refresh(kda(), layer=-1) == E.DASC_E_INVAL
     assert refresh(kda(), n_req=0) == E.DASC_E_INVAL
