@@ -188,16 +188,25 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   const __amdgpu_buffer_rsrc_t rk = rsrc(kp, W * D * 2), rv = rsrc(vp, W * D * 2);
   const __amdgpu_buffer_rsrc_t rg = rsrc(gp, PER_CHANNEL ? W * D * 4 : W * 4), rb = rsrc(bp, W * 4);
 
-  const int ch = tid & (D - 1);   // channel (or value column) owned in the load phases
-  const int hf = tid >> 7;        // which 16-token half of the chunk
+  // Load phase: lane pair (2 ch, 2 ch + 1) owns channel ch, the even lane tokens
+  // 0..15 of the chunk and the odd lane tokens 16..31, so the running sum of the gates
+  // crosses the halves with one lane shuffle.
+  const int ch = tid >> 1;
+  const int hf = tid & 1;
 
-  // Gates, keys and beta of one chunk as this thread loads them; the next chunk's are
-  // issued one chunk ahead.  Values are loaded at the top of each chunk (registers
-  // are the limit).
+  // Gates, keys, values and beta of one chunk as this thread loads them; the next
+  // chunk's are issued one chunk ahead.  Values come as column pairs: thread
+  // (octet o = tid / 64, pair p = tid % 64) holds columns 2p, 2p + 1 of tokens 8o .. 8o+7,
+  // so each load instruction reads one whole 256-byte token row.
+  const int vo = tid >> 6, vpair = tid & 63;
   float graw[16];
   uint4 kraw[2];
+  uint32_t vw[8];
   float braw;
   auto fetch = [&](int c0) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      vw[i] = __builtin_amdgcn_raw_buffer_load_b32(rv, ((8 * vo + i) * D + 2 * vpair) * 2, c0 * D * 2, 0);
 #pragma unroll
     for (int i = 0; i < 16; ++i)
       graw[i] = PER_CHANNEL ? ldf(rg, ((16 * hf + i) * D + ch) * 4, c0 * D * 4)
@@ -213,10 +222,6 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 
   for (int t0 = 0; t0 < W; t0 += C) {
     // ---- values of this chunk (issued first), then the prefetched gates, keys, beta ---
-    uint16_t vraw[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i)
-      vraw[i] = __builtin_amdgcn_raw_buffer_load_b16(rv, ((16 * hf + i) * D + ch) * 2, t0 * D * 2, 0);
     float Gl[16];
     {
       float run = 0.f;
@@ -225,33 +230,30 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         run += fmaxf(graw[i], kGateFloor) * kLog2e;
         Gl[i] = run;
       }
+      const float other = __shfl_xor(run, 1);   // every lane takes part
+      const float base = hf ? other : 0.f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) Gl[i] += base;
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
       *reinterpret_cast<uint4*>(sK + t * SK + c8) = kraw[u];
     }
-    {  // value column ch, tokens 16hf .. 16hf+15 -> one transposed row segment
-      uint32_t pk[8];
+    {  // columns 2p, 2p + 1, tokens 8o .. 8o+7 -> two transposed row segments
+      uint32_t lo[4], hi[4];
 #pragma unroll
-      for (int i = 0; i < 16; i += 2) pk[i >> 1] = uint32_t(vraw[i]) | (uint32_t(vraw[i + 1]) << 16);
-      uint4* dst = reinterpret_cast<uint4*>(sVT + ch * SV + 16 * hf);
-      dst[0] = make_uint4(pk[0], pk[1], pk[2], pk[3]);
-      dst[1] = make_uint4(pk[4], pk[5], pk[6], pk[7]);
+      for (int i = 0; i < 4; ++i) {
+        lo[i] = __builtin_amdgcn_perm(vw[2 * i + 1], vw[2 * i], 0x05040100u);  // low halves
+        hi[i] = __builtin_amdgcn_perm(vw[2 * i + 1], vw[2 * i], 0x07060302u);  // high halves
+      }
+      *reinterpret_cast<uint4*>(sVT + (2 * vpair) * SV + 8 * vo) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      *reinterpret_cast<uint4*>(sVT + (2 * vpair + 1) * SV + 8 * vo) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
     }
     if (tid < C) sBeta[tid] = braw;
 #pragma unroll
     for (int i = 0; i < 16; ++i) sG[(16 * hf + i) * SG + ch] = Gl[i];
-    __syncthreads();
-    if (hf == 1) {
-      const float base = sG[15 * SG + ch];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        Gl[i] += base;
-        sG[(16 + i) * SG + ch] = Gl[i];
-      }
-      sGam[ch] = ex2(Gl[15]);
-    }
+    if (hf) sGam[ch] = ex2(Gl[15]);
     __syncthreads();
 
     // ---- A = Diag(beta) (strictly lower part of R Q^T), three 16x16 tiles -----------
@@ -382,7 +384,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         }
       }
     }
-    __syncthreads();
+    // (no barrier: X below reads only K_G and this wave's registers)
 
     // ---- X = K_G S' on this wave's columns (rows t, contraction over channels) -------
     f32x4 X[2][2] = {};
@@ -407,6 +409,8 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         for (int nt = 0; nt < 2; ++nt) X[mu][nt] = mma3(ah, al, sh[nt], slo[nt], X[mu][nt]);
       }
     }
+
+    __syncthreads();   // T' complete
 
     // ---- U = T' (V - X): the difference stays in registers as the B operand --------
     f32x4 U[2][2];
