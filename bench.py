@@ -57,7 +57,7 @@ def parse():
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("pack_restore.hip", "quant.hip", "refresh.hip", "refresh_wy.hip",
+    for f in ("pack_restore.hip", "quant.hip", "refresh.hip", "refresh_wy.hip", "ckpt_layout.h",
               "refresh_kernels.h", "launch_common.h"):
         with open(os.path.join(ROOT, "paper_2608_30386_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
@@ -191,6 +191,22 @@ def bench_headline(torch, args):
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
 
+    # Load with refresh of the refreshed requests: dasc_restore + dasc_refresh (two launches)
+    # against the fused dasc_restore_refresh (one launch, the same result bit for bit)
+    def load_wr():
+        timer.run("restore_req", lambda: D.dasc_restore(sh, ckpt, req, inv_row, active, req, n_rows=R))
+        timer.run("refresh_req", lambda: D.dasc_refresh(sh, 0, inv_row, active, req, k, v, g, beta, W))
+        timer.run("restore_refresh", lambda: D.dasc_restore_refresh(
+            sh, 0, ckpt, req, inv_row, active, req, k, v, g, beta, W, n_rows=R))
+
+    load_wr()
+    torch.cuda.synchronize()
+    for name in ("restore_req", "refresh_req", "restore_refresh"):
+        timer.spans[name].clear()
+    for _ in range(args.steps):
+        load_wr()
+    torch.cuda.synchronize()
+
     omitted = (plan["inv_row"] < 0).reshape(sh.n_heads, sh.dk)
     heads_refreshed = int(omitted.any(axis=1).sum())
     bytes_pack = 2 * R * dv * 4 * n_ckpt
@@ -201,7 +217,11 @@ def bench_headline(torch, args):
     bytes_refresh = n_req * (heads_refreshed * per_head + int(omitted.sum()) * dv * 4)
     flops_refresh = WY_FLOP_PER_HEAD_TOKEN * W * n_req * heads_refreshed
 
-    t = {n: timer.mean_ms(n) for n in ("pack", "restore", "refresh")}
+    t = {n: timer.mean_ms(n) for n in ("pack", "restore", "refresh", "restore_req", "refresh_req",
+                                       "restore_refresh")}
+    # fused: suffix inputs of every refreshed head, each kept row read once, every row of
+    # the layer written once
+    bytes_fused = n_req * (heads_refreshed * (per_head - 4 * sh.dk * dv) + R * dv * 4 + rows * dv * 4)
     kernels = {
         "pack": {"ms": t["pack"], "GBps": bytes_pack / t["pack"] / 1e6,
                  "hbm_frac": bytes_pack / t["pack"] / 1e6 / HBM_PEAK_GBPS, "bytes": bytes_pack},
@@ -212,6 +232,10 @@ def bench_headline(torch, args):
                     "GBps": bytes_refresh / t["refresh"] / 1e6,
                     "TFLOPs": flops_refresh / t["refresh"] / 1e9, "bytes": bytes_refresh,
                     "flops": flops_refresh, "heads": n_req * heads_refreshed},
+        "restore_refresh_fused": {
+            "ms": t["restore_refresh"], "unfused_ms": t["restore_req"] + t["refresh_req"],
+            "requests": n_req, "GBps": bytes_fused / t["restore_refresh"] / 1e6,
+            "bytes": bytes_fused},
     }
     achieved = bytes_refresh / t["refresh"] / 1e6          # GB/s
     traffic = measured_traffic("kimi_headline/refresh")

@@ -247,13 +247,43 @@ int dasc_refresh_workspace_bytes(const dasc_shape *shape, int32_t n_req, int32_t
  *   workspace: device, at least dasc_refresh_workspace_bytes (may be NULL if that is 0).
  * Arithmetic is fp32 with bf16 inputs widened exactly.
  * Errors: DASC_E_INVAL (NULL pointer, misalignment, layer out of [0, L), n_req < 1,
- * W < 1 or W > DASC_MAX_WINDOW, bad init_mode, n_pool < 1), DASC_E_SHAPE (bad shape), DASC_E_WORKSPACE,
- * DASC_E_UNSUPPORTED (dk not in {16, 32, 64, 128} or dv > 256), DASC_E_HIP. */
+ * W < 1 or W > DASC_MAX_WINDOW, bad init_mode, n_pool < 1), DASC_E_SHAPE (bad shape),
+ * DASC_E_WORKSPACE, DASC_E_UNSUPPORTED (dk not in {16, 32, 64, 128} or dv > 256),
+ * DASC_E_HIP. */
 int dasc_refresh(const dasc_shape *shape, int32_t layer, const int32_t *inv_row,
                  float *states, int64_t n_pool, const int32_t *slot,
                  const uint16_t *k, const uint16_t *v, const float *g, const float *beta,
                  int32_t n_req, int32_t W, int32_t init_mode,
                  void *workspace, size_t workspace_bytes, dasc_stream_t stream);
+
+/* ---- Load with refresh, fused (Sec. 4.2: restore, then DASC-WR) ----------- */
+
+/* One launch doing what dasc_restore followed by dasc_refresh does for one layer:
+ * for each request i < n_req, the rows of layer `layer` of states[dst_slot[i]] receive
+ *   - omitted rows of heads that have any (KDA rows; GDN whole heads): S'_W of the
+ *     replay above, started from the restored head (kept rows taken from checkpoint
+ *     src_slot[i], omitted rows +0.0) or from zero (DASC_INIT_ZERO);
+ *   - every other row: its packed row of checkpoint src_slot[i], bit for bit (+0.0 if
+ *     inv_row points outside [0, n_rows)).
+ * The state is read from the checkpoint, never from `states`; every row of the layer
+ * is written once and rows of other layers are not touched.  The result equals
+ * dasc_restore (of this layer) followed by dasc_refresh bit for bit.
+ *   ckpt, n_ckpt_slots, n_ranks, slice_rows, n_rows, inv_row: as in dasc_restore.
+ *   src_slot: device int32 [n_req], checkpoint slot per request.
+ *   states, dst_slot: as states, slot in dasc_refresh (the pool need not hold the
+ *   restored state beforehand).
+ *   k, v, g, beta, W, init_mode, workspace: as in dasc_refresh.
+ * Built for dk = dv = 128 (the shapes of Sec. 5.1).
+ * Errors: those of dasc_restore and dasc_refresh; DASC_E_UNSUPPORTED unless
+ * dk = dv = 128. */
+int dasc_restore_refresh(const dasc_shape *shape, int32_t layer,
+                         const float *ckpt, int64_t n_ckpt_slots, const int32_t *src_slot,
+                         int32_t n_ranks, int64_t slice_rows, int64_t n_rows,
+                         const int32_t *inv_row, float *states, int64_t n_pool,
+                         const int32_t *dst_slot,
+                         const uint16_t *k, const uint16_t *v, const float *g, const float *beta,
+                         int32_t n_req, int32_t W, int32_t init_mode,
+                         void *workspace, size_t workspace_bytes, dasc_stream_t stream);
 
 #ifdef __cplusplus
 }

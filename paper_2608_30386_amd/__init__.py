@@ -17,5 +17,6 @@ from .dasc import (  # noqa: F401
     dasc_refresh_workspace_bytes,
     dasc_restore,
     dasc_restore_q8,
+    dasc_restore_refresh,
     dasc_static_log_decay,
 )

@@ -30,7 +30,7 @@ DASC_INIT_ZERO = 1
 EXPORTED = (
     "dasc_static_log_decay", "dasc_plan", "dasc_matched_slots", "dasc_strerror",
     "dasc_pack", "dasc_restore", "dasc_pack_q8", "dasc_restore_q8",
-    "dasc_refresh_workspace_bytes", "dasc_refresh",
+    "dasc_refresh_workspace_bytes", "dasc_refresh", "dasc_restore_refresh",
 )
 
 
@@ -94,6 +94,8 @@ def _load() -> C.CDLL:
         "dasc_restore_q8": [C.POINTER(Shape), P, P, I64, P, I64, P, P, I64, P, I32, P],
         "dasc_refresh_workspace_bytes": [C.POINTER(Shape), I32, I32, C.POINTER(C.c_size_t)],
         "dasc_refresh": [C.POINTER(Shape), I32, P, P, I64, P, P, P, P, P, I32, I32, I32, P, SZ, P],
+        "dasc_restore_refresh": [C.POINTER(Shape), I32, P, I64, P, I32, I64, I64, P, P, I64, P,
+                                 P, P, P, P, I32, I32, I32, P, SZ, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)

@@ -1,0 +1,20 @@
+// Device-side addressing of the packed checkpoint layout, shared by the kernels that
+// read or write it.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace dasc {
+
+// Row offset (in rows) of packed row j of checkpoint slot `slot` in the
+// [T, n_slots, slice_rows] layout of Sec. 4.3 (rank r holds packed rows
+// [r * slice_rows, (r + 1) * slice_rows)); the flat layout (one slice) needs no division.
+__device__ inline int64_t slice_row(int64_t j, int64_t slice_rows, int64_t n_rows,
+                                    int64_t n_slots, int64_t slot) {
+  const int64_t r = slice_rows >= n_rows ? 0 : int64_t(uint32_t(j) / uint32_t(slice_rows));
+  return (r * n_slots + slot) * slice_rows + (j - r * slice_rows);
+}
+
+}  // namespace dasc

@@ -19,6 +19,7 @@
 #include <cstdint>
 
 #include "dasc.h"
+#include "ckpt_layout.h"
 #include "launch_common.h"
 
 namespace {
@@ -44,13 +45,7 @@ struct RowGeom<-1> {
   __device__ static int col_of(int v, int rt) { return v % rt; }
 };
 
-// Row offset (in rows) of packed row j of checkpoint slot `slot` in the
-// [T, n_slots, slice_rows] layout; the flat layout (one slice) needs no division.
-__device__ inline int64_t slice_row(int64_t j, int64_t slice_rows, int64_t n_rows,
-                                    int64_t n_slots, int64_t slot) {
-  const int64_t r = slice_rows >= n_rows ? 0 : int64_t(uint32_t(j) / uint32_t(slice_rows));
-  return (r * n_slots + slot) * slice_rows + (j - r * slice_rows);
-}
+using dasc::slice_row;
 
 // Rows per block: enough 128-bit vectors for every thread to move kUnroll of them.
 inline int rows_per_block(int vpr) { return vpr >= kVecPerBlock ? 1 : kVecPerBlock / vpr; }

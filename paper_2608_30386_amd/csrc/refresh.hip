@@ -175,3 +175,43 @@ extern "C" int dasc_refresh(const dasc_shape* shape, int32_t layer, const int32_
   }
   return dasc::launch_status();
 }
+
+extern "C" int dasc_restore_refresh(const dasc_shape* shape, int32_t layer, const float* ckpt,
+                                    int64_t n_ckpt_slots, const int32_t* src_slot,
+                                    int32_t n_ranks, int64_t slice_rows, int64_t n_rows,
+                                    const int32_t* inv_row, float* states, int64_t n_pool,
+                                    const int32_t* dst_slot, const uint16_t* k,
+                                    const uint16_t* v, const float* g, const float* beta,
+                                    int32_t n_req, int32_t W, int32_t init_mode,
+                                    void* workspace, size_t workspace_bytes,
+                                    dasc_stream_t stream) {
+  if (!shape) return DASC_E_INVAL;
+  if (!dasc::valid_shape(shape) || shape->dv % 4 != 0) return DASC_E_SHAPE;
+  if (layer < 0 || layer >= shape->n_layers || n_req < 1 || W < 1 || W > DASC_MAX_WINDOW ||
+      n_pool < 1 || n_ckpt_slots < 1 || n_ranks < 1 || n_rows < 0)
+    return DASC_E_INVAL;
+  if (n_rows > dasc::rows_per_state(shape)) return DASC_E_SHAPE;
+  if (n_rows > 0 && (slice_rows < 1 || slice_rows > INT32_MAX || slice_rows * n_ranks < n_rows))
+    return DASC_E_INVAL;
+  if (init_mode != DASC_INIT_RESTORED && init_mode != DASC_INIT_ZERO) return DASC_E_INVAL;
+  if (!inv_row || !states || !src_slot || !dst_slot || !k || !v || !g || !beta)
+    return DASC_E_INVAL;
+  if (n_rows > 0 && !ckpt) return DASC_E_INVAL;
+  if (!dasc::aligned16(states) || !dasc::aligned16(ckpt) || !dasc::aligned16(k) ||
+      !dasc::aligned16(v))
+    return DASC_E_INVAL;
+  size_t need = 0;
+  int rc = dasc_refresh_workspace_bytes(shape, n_req, W, &need);
+  if (rc != DASC_OK) return rc;
+  if (workspace_bytes < need || (need > 0 && !workspace)) return DASC_E_WORKSPACE;
+  if (!dasc::refresh_wy_supported(shape->dk, shape->dv)) return DASC_E_UNSUPPORTED;
+  if (int64_t(n_req) * shape->n_heads > INT32_MAX) return DASC_E_INVAL;
+  if (n_rows == 0) slice_rows = 1;  // nothing is read; keeps the divisor non-zero
+  (void)hipGetLastError();
+  dasc::launch_restore_refresh_wy(shape->arch == DASC_ARCH_KDA, n_req, shape->n_heads,
+                                  shape->n_qk_heads, layer, shape->n_layers, ckpt, n_ckpt_slots,
+                                  src_slot, slice_rows, n_rows, inv_row, states, n_pool, dst_slot,
+                                  k, v, g, beta, W, init_mode == DASC_INIT_ZERO,
+                                  reinterpret_cast<hipStream_t>(stream));
+  return dasc::launch_status();
+}

@@ -14,4 +14,14 @@ void launch_refresh_wy(bool per_channel, int n_req, int H, int Hqk, int layer, i
                        const uint16_t* k, const uint16_t* v, const float* g, const float* beta,
                        int W, int init_zero, hipStream_t st);
 
+// The same kernel fused with the restore of the layer: the initial state of each head is
+// read from the packed checkpoint (kept rows; omitted rows start at zero) and every row
+// of the layer is written (omitted rows refreshed, kept rows copied bit for bit).
+void launch_restore_refresh_wy(bool per_channel, int n_req, int H, int Hqk, int layer, int L,
+                               const float* ckpt, int64_t n_ckpt_slots, const int32_t* ck_slot,
+                               int64_t slice_rows, int64_t n_rows, const int32_t* inv_row,
+                               float* states, int64_t n_pool, const int32_t* slot,
+                               const uint16_t* k, const uint16_t* v, const float* g,
+                               const float* beta, int W, int init_zero, hipStream_t st);
+
 }  // namespace dasc

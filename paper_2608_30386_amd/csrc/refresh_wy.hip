@@ -38,11 +38,22 @@
 // floored at -10 (a decay of 4.5e-5 per token instead of anything smaller), which
 // keeps every factor below e^80 in fp32 and changes the state by at most 4.5e-5 of
 // its magnitude per floored token.
+//
+// Fused with the restore (FUSED = true), the initial state of a head is read from the
+// packed checkpoint instead of the active state (kept rows from their packed position,
+// omitted rows +0.0), and every row of the layer is written: kept rows, copied bit for
+// bit from the checkpoint, as soon as they are read (they overlap the replay), omitted
+// rows from the replay at the end.  A head with no omitted row is a plain copy.  The arithmetic is the unfused kernel's, so the result
+// equals restore followed by refresh bit for bit.
+//
+// Inputs are read through raw buffer resources sized to one head's window, so tokens
+// past the window load as zeros: k = v = 0, g = 0, beta = 0, an identity step.
 
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 
+#include "ckpt_layout.h"
 #include "refresh_kernels.h"
 
 namespace {
@@ -135,12 +146,19 @@ __device__ inline bf16x8 cat(bf16x4 a, bf16x4 b) {
   return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
 }
 
-template <bool PER_CHANNEL>
+// Packed checkpoint of the fused variant (unused when FUSED is false).
+struct CkptView {
+  const float* ckpt;
+  int64_t n_slots, slice_rows, n_rows;
+  const int32_t* slot;   // checkpoint slot per request
+};
+
+template <bool PER_CHANNEL, bool FUSED>
 __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     int H, int Hqk, int layer, int L, const int32_t* __restrict__ inv_row,
     float* __restrict__ states, int64_t n_pool, const int32_t* __restrict__ slot,
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, const float* __restrict__ g,
-    const float* __restrict__ beta, int W, int init_zero) {
+    const float* __restrict__ beta, int W, int init_zero, CkptView ck) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
   float* sG = reinterpret_cast<float*>(smem + OFF_G);
   uint16_t* sK = reinterpret_cast<uint16_t*>(smem + OFF_K);
@@ -165,10 +183,42 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   const int64_t head_row = (int64_t(layer) * H + h) * D;
   bool mine = false;
   if (tid < D) mine = inv_row[head_row + tid] < 0;
-  if (!__syncthreads_or(mine)) return;
+  const bool any_omitted = __syncthreads_or(mine);
+  if (!FUSED && !any_omitted) return;
   const int64_t sl = slot[n];
   if (sl < 0 || sl >= n_pool) return;
   float* S_head = states + (sl * L * H * D + head_row) * D;
+  int64_t cslot = 0;
+  if (FUSED) {
+    cslot = ck.slot[n];
+    if (cslot < 0 || cslot >= ck.n_slots) return;
+  }
+  // Fused: where dense row c of this head sits in the checkpoint, as a float offset
+  // (kOmitted for an omitted row, kNoRow for an index outside the packed rows, which
+  // restores as +0.0).  One thread per row fills the table in the A buffer, which is
+  // free until the first chunk.
+  constexpr int64_t kOmitted = -1, kNoRow = -2;
+  int64_t* sOff = reinterpret_cast<int64_t*>(smem + OFF_A);
+  static_assert(D * 8 <= C * C * 4, "row table must fit in the A buffer");
+  if (FUSED) {
+    if (tid < D) {
+      const int64_t p = inv_row[head_row + tid];
+      sOff[tid] = p < 0 ? kOmitted
+                : p >= ck.n_rows ? kNoRow
+                : dasc::slice_row(p, ck.slice_rows, ck.n_rows, ck.n_slots, cslot) * D;
+    }
+    __syncthreads();
+  }
+  if (FUSED && !any_omitted) {   // nothing to replay: restore the head as it is
+    for (int e = tid; e < D * D / 4; e += 256) {
+      const int c = e >> 5, v4 = e & 31;
+      const int64_t o = sOff[c];
+      const f32x4 val = o >= 0 ? reinterpret_cast<const f32x4*>(ck.ckpt + o)[v4]
+                               : f32x4{0.f, 0.f, 0.f, 0.f};
+      reinterpret_cast<f32x4*>(S_head + int64_t(c) * D)[v4] = val;
+    }
+    return;
+  }
 
   // S'[c][j] for c = 16 mt + 4q + i, j = 32w + 16 nt + r
   f32x4 S[8][2];
@@ -177,8 +227,19 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        S[mt][nt][i] = init_zero ? 0.f : S_head[int64_t(16 * mt + 4 * q + i) * D + 32 * w + 16 * nt + r];
+      for (int i = 0; i < 4; ++i) {
+        const int c = 16 * mt + 4 * q + i, j = 32 * w + 16 * nt + r;
+        if (FUSED) {
+          // the restored value; a kept row is final already and is stored right away,
+          // while the replay runs
+          const int64_t o = sOff[c];
+          const float val = o >= 0 ? ck.ckpt[o + j] : 0.f;
+          S[mt][nt][i] = init_zero ? 0.f : val;
+          if (o != kOmitted) S_head[int64_t(c) * D + j] = val;
+        } else {
+          S[mt][nt][i] = init_zero ? 0.f : S_head[int64_t(c) * D + j];
+        }
+      }
 
   const int hk = h / (H / Hqk);
   const uint16_t* kp = k + (int64_t(n) * Hqk + hk) * W * D;
@@ -470,7 +531,9 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int c = 16 * mt + 4 * q + i;
-      if (inv_row[head_row + c] < 0) {
+      // re-read (volatile): merged with the loads of the start, 32 predicates would stay
+      // live through the replay and spill
+      if (reinterpret_cast<const volatile int32_t*>(inv_row)[head_row + c] < 0) {
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) S_head[int64_t(c) * D + 32 * w + 16 * nt + r] = S[mt][nt][i];
       }
@@ -488,12 +551,29 @@ void launch_refresh_wy(bool per_channel, int n_req, int H, int Hqk, int layer, i
                        const uint16_t* k, const uint16_t* v, const float* g, const float* beta,
                        int W, int init_zero, hipStream_t st) {
   const dim3 grid(unsigned(n_req) * unsigned(H)), block(256);
+  const CkptView none{nullptr, 1, 1, 0, nullptr};
   if (per_channel)
-    hipLaunchKernelGGL(refresh_wy_kernel<true>, grid, block, 0, st, H, Hqk, layer, L, inv_row,
-                       states, n_pool, slot, k, v, g, beta, W, init_zero);
+    hipLaunchKernelGGL((refresh_wy_kernel<true, false>), grid, block, 0, st, H, Hqk, layer, L,
+                       inv_row, states, n_pool, slot, k, v, g, beta, W, init_zero, none);
   else
-    hipLaunchKernelGGL(refresh_wy_kernel<false>, grid, block, 0, st, H, Hqk, layer, L, inv_row,
-                       states, n_pool, slot, k, v, g, beta, W, init_zero);
+    hipLaunchKernelGGL((refresh_wy_kernel<false, false>), grid, block, 0, st, H, Hqk, layer, L,
+                       inv_row, states, n_pool, slot, k, v, g, beta, W, init_zero, none);
+}
+
+void launch_restore_refresh_wy(bool per_channel, int n_req, int H, int Hqk, int layer, int L,
+                               const float* ckpt, int64_t n_ckpt_slots, const int32_t* ck_slot,
+                               int64_t slice_rows, int64_t n_rows, const int32_t* inv_row,
+                               float* states, int64_t n_pool, const int32_t* slot,
+                               const uint16_t* k, const uint16_t* v, const float* g,
+                               const float* beta, int W, int init_zero, hipStream_t st) {
+  const dim3 grid(unsigned(n_req) * unsigned(H)), block(256);
+  const CkptView ck{ckpt, n_ckpt_slots, slice_rows, n_rows, ck_slot};
+  if (per_channel)
+    hipLaunchKernelGGL((refresh_wy_kernel<true, true>), grid, block, 0, st, H, Hqk, layer, L,
+                       inv_row, states, n_pool, slot, k, v, g, beta, W, init_zero, ck);
+  else
+    hipLaunchKernelGGL((refresh_wy_kernel<false, true>), grid, block, 0, st, H, Hqk, layer, L,
+                       inv_row, states, n_pool, slot, k, v, g, beta, W, init_zero, ck);
 }
 
 }  // namespace dasc

@@ -241,3 +241,37 @@ def dasc_refresh(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta,
         _dev(k, torch.bfloat16, "k"), _dev(v, torch.bfloat16, "v"),
         _dev(g, torch.float32, "g"), _dev(beta, torch.float32, "beta"),
         slot.numel(), W, INIT[init_mode], ws_ptr, ws_bytes, _stream(stream)), "dasc_refresh")
+
+
+def dasc_restore_refresh(shape: Shape, layer: int, ckpt, src_slot, inv_row, states, dst_slot,
+                         k, v, g, beta, W: int, n_rows: int, n_ranks: int = 1,
+                         slice_rows: int | None = None, init_mode: str = "restored",
+                         workspace=None, stream=None) -> None:
+    """Restore one layer of each request's state from its checkpoint and refresh its
+    omitted units in one launch (dk = dv = 128).  Arguments as dasc_restore and
+    dasc_refresh; request i reads checkpoint src_slot[i] and writes pool slot dst_slot[i].
+    """
+    import torch
+
+    n_req, H, dk, dv = src_slot.numel(), shape.n_heads, shape.dk, shape.dv
+    slice_rows = n_rows if slice_rows is None else slice_rows
+    n_slots = ckpt.shape[1] if ckpt.dim() == 4 else ckpt.shape[0]
+    _need(ckpt, n_ranks * n_slots * slice_rows * dv, "ckpt")
+    _need(states, states.shape[0] * shape.rows * dv, "states")
+    _need(inv_row, shape.rows, "inv_row")
+    _need(dst_slot, n_req, "dst_slot")
+    _need(k, n_req * shape.n_qk_heads * W * dk, "k")
+    _need(v, n_req * H * W * dv, "v")
+    _need(g, n_req * H * W * (dk if shape.arch == "kda" else 1), "g")
+    _need(beta, n_req * H * W, "beta")
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        ws_ptr, ws_bytes = _dev(workspace, torch.uint8, "workspace"), workspace.numel()
+    _check(LIB.dasc_restore_refresh(
+        C.byref(shape.c()), layer, _dev(ckpt, torch.float32, "ckpt"), n_slots,
+        _dev(src_slot, torch.int32, "src_slot"), n_ranks, slice_rows, n_rows,
+        _dev(inv_row, torch.int32, "inv_row"), _dev(states, torch.float32, "states"),
+        states.shape[0], _dev(dst_slot, torch.int32, "dst_slot"),
+        _dev(k, torch.bfloat16, "k"), _dev(v, torch.bfloat16, "v"),
+        _dev(g, torch.float32, "g"), _dev(beta, torch.float32, "beta"),
+        n_req, W, INIT[init_mode], ws_ptr, ws_bytes, _stream(stream)), "dasc_restore_refresh")

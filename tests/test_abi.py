@@ -25,11 +25,46 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     assert set(names) == set(_lib.EXPORTED)
     lib = C.CDLL(_lib.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
+
+
+def restore_refresh(shape, layer=0, W=8, n_req=1, init=0, ptrs=None, n_rows=4, n_slots=1, T=1,
+                    slice_rows=4, n_pool=1, ws=None, ws_bytes=0):
+    p = dict(ckpt=FAKE, src=FAKE, inv=FAKE, states=FAKE, dst=FAKE, k=FAKE, v=FAKE, g=FAKE,
+             beta=FAKE)
+    p.update(ptrs or {})
+    return LIB.dasc_restore_refresh(C.byref(shape) if shape is not None else None, layer,
+                                    p["ckpt"], n_slots, p["src"], T, slice_rows, n_rows, p["inv"],
+                                    p["states"], n_pool, p["dst"], p["k"], p["v"], p["g"],
+                                    p["beta"], n_req, W, init, ws, ws_bytes, None)
+
+
+def test_restore_refresh_argument_errors():
+    E = _lib
+    assert restore_refresh(None) == E.DASC_E_INVAL
+    assert restore_refresh(kda(dv=6)) == E.DASC_E_SHAPE
+    assert restore_refresh(kda(), layer=2) == E.DASC_E_INVAL
+    assert restore_refresh(kda(), W=0) == E.DASC_E_INVAL
+    assert restore_refresh(kda(), W=E.DASC_MAX_WINDOW + 1) == E.DASC_E_INVAL
+    assert restore_refresh(kda(), n_req=0) == E.DASC_E_INVAL
+    assert restore_refresh(kda(), init=5) == E.DASC_E_INVAL
+    assert restore_refresh(kda(), n_slots=0) == E.DASC_E_INVAL
+    assert restore_refresh(kda(), T=0) == E.DASC_E_INVAL
+    assert restore_refresh(kda(), n_pool=0) == E.DASC_E_INVAL
+    assert restore_refresh(kda(), n_rows=9, T=2, slice_rows=4) == E.DASC_E_INVAL
+    assert restore_refresh(kda(L=1, H=1, dk=4, dv=4), n_rows=5) == E.DASC_E_SHAPE
+    for name in ("ckpt", "src", "inv", "states", "dst", "k", "v", "g", "beta"):
+        assert restore_refresh(kda(), ptrs={name: None}) == E.DASC_E_INVAL, name
+    assert restore_refresh(kda(), ptrs={"ckpt": None}, n_rows=0) == E.DASC_E_UNSUPPORTED
+    for name in ("ckpt", "states", "k", "v"):
+        assert restore_refresh(kda(), ptrs={name: FAKE_ODD}) == E.DASC_E_INVAL, name
+    # every argument valid: only dk = dv = 128 has a fused kernel
+    assert restore_refresh(kda()) == E.DASC_E_UNSUPPORTED
+    assert restore_refresh(kda(dk=128, dv=64)) == E.DASC_E_UNSUPPORTED
 
 
 def test_strerror_total():
