@@ -8,6 +8,7 @@ Follows, in order:
   App. B, Scheme 2  ragged layout: layer l owns [o_l, o_{l+1}), o_0 = 0, o_{l+1} = o_l + r_l
   Sec. 4.2, Eq. 7   W_u = clamp(next_pow2(H_s(u)), 4, W_max), W_replay = max over omitted u
   Sec. 4.3          per-rank slot width C = ceil(sum_r U_r / T)
+  Sec. 4.3 stage 1  load-time head-bundle permutation across TP ranks (tp_permutation)
   Sec. 4.1, Eq. 6   C_temp^rag, C_ckpt^rag; padded C_temp^pad and layout gain R_max / r_bar
   App. C.1, Eq. 8   matched-HBM slot count N = floor(B / b_bottleneck) - 1
 
@@ -20,7 +21,13 @@ Readings where the paper is silent (each also listed in the design notes):
   * next_pow2(x) is the smallest power of two >= x; the clamp's upper end is W_max;
   * owner (compute) rank of head h under TP degree T is floor(h * T / H); storage
     rank of packed unit p is floor(p / C);
-  * the per-rank bottleneck in Eq. 6 / Eq. 8 is the balanced slot width C units.
+  * the per-rank bottleneck in Eq. 6 / Eq. 8 is the balanced slot width C units;
+  * stage-1 permutation (no algorithm given): a bundle is one query/key head with the
+    H/Hqk value heads that share it; longest-processing-time placement, bundles by
+    retained rows descending (ties: lower layer, then lower bundle) onto the least
+    loaded rank (ties: lower rank) that still has room for it in that layer (every
+    rank holds Hqk/T bundles of every layer); the identity is kept whenever it is no
+    worse, so the worst rank never grows.
 
 All arithmetic is binary64; transcendental calls go through Python's ``math``
 module (the platform libm) one element at a time.
@@ -226,3 +233,59 @@ def matched_slots(budget_bytes: int, bottleneck_slot_bytes: int) -> int:
     if bottleneck_slot_bytes <= 0:
         raise ValueError("slot bytes must be positive")
     return budget_bytes // bottleneck_slot_bytes - 1
+
+
+def tp_permutation(unit_count: np.ndarray, arch: str, n_qk_heads: int, n_ranks: int,
+                   dk: int) -> dict:
+    """Sec. 4.3, stage 1: a model-load-time reindexing of linear-attention head bundles
+    across the T tensor-parallel ranks, chosen so that the most loaded rank holds as few
+    retained rows as possible (the number of resident checkpoints is limited by it).
+
+    unit_count: [L, H] retained units per (layer, head) (KDA: rows; GDN: 0 or 1 heads).
+    Rank r computes bundle positions [r * Hqk/T, (r + 1) * Hqk/T) of every layer.
+    Returns head_perm [L, H] (head_perm[l, p] = original head now at position p; the
+    heads of a bundle stay consecutive and in order), rank_rows [T] after the
+    permutation and rank_rows_identity [T] before it.
+    """
+    L, H = unit_count.shape
+    B, T = n_qk_heads, n_ranks
+    if H % B != 0 or B % T != 0:
+        raise ValueError("heads must split into bundles, bundles evenly over ranks")
+    g, cap = H // B, B // T
+    rows_per_unit = 1 if arch == "kda" else dk
+    load = [[sum(int(unit_count[l, b * g + i]) for i in range(g)) * rows_per_unit
+             for b in range(B)] for l in range(L)]
+
+    ident = [0] * T
+    for l in range(L):
+        for b in range(B):
+            ident[b // cap] += load[l][b]
+
+    order = sorted(((l, b) for l in range(L) for b in range(B)),
+                   key=lambda lb: (-load[lb[0]][lb[1]], lb[0], lb[1]))
+    U = [0] * T
+    used = [[0] * T for _ in range(L)]
+    owner = [[0] * B for _ in range(L)]
+    for l, b in order:
+        best = -1
+        for r in range(T):
+            if used[l][r] < cap and (best < 0 or U[r] < U[best]):
+                best = r
+        owner[l][b] = best
+        used[l][best] += 1
+        U[best] += load[l][b]
+
+    if max(U) >= max(ident):          # no better than the identity: keep it
+        owner = [[b // cap for b in range(B)] for _ in range(L)]
+        U = list(ident)
+    perm = np.zeros((L, H), dtype=np.int64)
+    for l in range(L):
+        pos = 0
+        for r in range(T):
+            for b in range(B):          # a rank's bundles in their original order
+                if owner[l][b] == r:
+                    for i in range(g):
+                        perm[l, pos] = b * g + i
+                        pos += 1
+    return {"head_perm": perm, "rank_rows": np.array(U, dtype=np.int64),
+            "rank_rows_identity": np.array(ident, dtype=np.int64)}

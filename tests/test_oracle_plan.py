@@ -203,3 +203,102 @@ def test_matched_hbm_slots_golden():
         assert p["slot_bytes_rank"] == per_slot
         assert P.matched_slots(b, p["slot_bytes_rank"]) == 127
         assert p["c_ckpt"] == 1.0
+
+
+# ---- Sec. 4.3 stage 1: head-bundle permutation across TP ranks -------------------------
+
+def _bundle_loads(unit_count, arch, B, dk):
+    L, H = unit_count.shape
+    g, rpu = H // B, (1 if arch == "kda" else dk)
+    return [[int(unit_count[l, b * g:(b + 1) * g].sum()) * rpu for b in range(B)] for l in range(L)]
+
+
+def _check_permutation(unit_count, arch, B, T, dk, res):
+    """head_perm moves whole bundles, gives every rank B/T bundles per layer, and the
+    reported per-rank rows are what the permuted placement holds."""
+    L, H = unit_count.shape
+    g, cap = H // B, B // T
+    rpu = 1 if arch == "kda" else dk
+    perm = res["head_perm"]
+    rows = [0] * T
+    for l in range(L):
+        assert sorted(perm[l].tolist()) == list(range(H))
+        for pos_b in range(B):
+            heads = perm[l, pos_b * g:(pos_b + 1) * g].tolist()
+            assert heads[0] % g == 0 and heads == list(range(heads[0], heads[0] + g))
+            rows[pos_b // cap] += int(unit_count[l, heads].sum()) * rpu
+    assert rows == res["rank_rows"].tolist()
+    ident = [0] * T
+    for l in range(L):
+        for b, x in enumerate(_bundle_loads(unit_count, arch, B, dk)[l]):
+            ident[b // cap] += x
+    assert ident == res["rank_rows_identity"].tolist()
+
+
+def _optimum(loads, T, cap):
+    """Smallest worst-rank load over every placement with B/T bundles per rank per layer
+    (brute force; tiny inputs only)."""
+    import itertools
+
+    L, B = len(loads), len(loads[0])
+    per_layer = []
+    for l in range(L):
+        opts = set()
+        for owner in itertools.product(range(T), repeat=B):
+            if all(owner.count(r) == cap for r in range(T)):
+                opts.add(tuple(sum(loads[l][b] for b in range(B) if owner[b] == r) for r in range(T)))
+        per_layer.append(sorted(opts))
+    best = None
+    for combo in itertools.product(*per_layer):
+        worst = max(sum(c[r] for c in combo) for r in range(T))
+        best = worst if best is None else min(best, worst)
+    return best
+
+
+def test_tp_permutation_hand_worked():
+    # Two KDA layers, four heads, T = 2 (two heads per rank and layer).  Retained rows
+    # [8, 1, 1, 0] and [8, 0, 0, 0]: the identity puts 8 + 1 + 8 = 17 rows on rank 0 and
+    # 1 on rank 1.  Largest first: (0, 0) -> rank 0, (1, 0) -> rank 1 (now 8 / 8),
+    # (0, 1) -> rank 0 (tie, lower rank), (0, 2) -> rank 1, the empty bundles fill the
+    # remaining places: 9 / 9 rows, the optimum (18 rows over two ranks).
+    uc = np.array([[8, 1, 1, 0], [8, 0, 0, 0]])
+    res = P.tp_permutation(uc, "kda", 4, 2, 16)
+    assert res["rank_rows"].tolist() == [9, 9]
+    assert res["rank_rows_identity"].tolist() == [17, 1]
+    assert res["head_perm"].tolist() == [[0, 1, 2, 3], [1, 2, 0, 3]]
+    _check_permutation(uc, "kda", 4, 2, 16, res)
+
+
+def test_tp_permutation_trivial_cases():
+    rng = np.random.default_rng(3)
+    uc = rng.integers(0, 17, size=(3, 8))
+    one = P.tp_permutation(uc, "kda", 8, 1, 16)            # one rank: nothing to move
+    assert one["head_perm"].tolist() == [list(range(8))] * 3
+    assert one["rank_rows"].tolist() == [int(uc.sum())]
+    flat = P.tp_permutation(np.full((2, 8), 5), "kda", 8, 4, 16)   # already balanced
+    assert flat["head_perm"].tolist() == [list(range(8))] * 2
+    assert flat["rank_rows"].tolist() == [20, 20, 20, 20]
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_tp_permutation_brute_force(seed):
+    rng = np.random.default_rng(100 + seed)
+    arch = "kda" if seed % 2 == 0 else "gdn"
+    L, T = (2, 2) if seed % 3 else (1, 3)
+    B = 4 if T == 2 else 6
+    g = 1 if arch == "kda" else 2                           # value heads per bundle
+    hi = 17 if arch == "kda" else 2
+    uc = rng.integers(0, hi, size=(L, B * g))
+    if seed % 4 == 1:
+        uc[0, :g] = hi - 1                                   # one heavy bundle
+    res = P.tp_permutation(uc, arch, B, T, 16)
+    _check_permutation(uc, arch, B, T, 16, res)
+    loads = _bundle_loads(uc, arch, B, 16)
+    opt = _optimum(loads, T, B // T)
+    worst = max(res["rank_rows"])
+    assert opt <= worst <= max(res["rank_rows_identity"])
+    # placing items largest first onto the least loaded rank is optimal when no bundle
+    # exceeds a third of the balanced load (the classic LPT bound is then tight here)
+    total = sum(map(sum, loads))
+    if max(map(max, loads)) * 3 <= total / T and B // T >= 2:
+        assert worst <= opt + max(map(max, loads)) // 3
