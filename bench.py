@@ -376,8 +376,22 @@ def bench_pack_restore_only(torch, args, name):
                     for tt, k_, b in ((t, "pack", bp), (t, "restore", br),
                                       (tq, "pack_q8", bpq), (tq, "restore_q8", brq))},
         "q8_checkpoint_bytes": R * (dv + 4), "fp32_checkpoint_bytes": R * dv * 4,
+        "tp_stage1": tp_stage1(D, sh, plan, T),
         "plan_host_ms": plan_s * 1e3,
     }
+
+
+def tp_stage1(D, sh, plan, T):
+    """Stage-1 head-bundle permutation on this plan (host): retained rows of the worst
+    rank before and after, and the rows stage 2 must move off over-full ranks to reach
+    the balanced slot width C (rows a rank owns beyond C)."""
+    res = D.dasc_tp_permutation(sh, plan["unit_count"], T)
+    C = -(-int(plan["n_rows"]) // T)
+    over = lambda rows: int(np.maximum(rows - C, 0).sum())  # noqa: E731
+    return {"worst_rank_rows_identity": int(res["rank_rows_identity"].max()),
+            "worst_rank_rows_permuted": int(res["rank_rows"].max()), "balanced_rows": C,
+            "moved_rows_identity": over(res["rank_rows_identity"]),
+            "moved_rows_permuted": over(res["rank_rows"])}
 
 
 def bench_gdn(torch, args):

@@ -150,6 +150,26 @@ int dasc_plan(const dasc_plan_desc *desc, const double *g_static, dasc_plan_out 
  * reserved).  Errors: DASC_E_INVAL if slots is NULL, budget_bytes < 0 or slot_bytes <= 0. */
 int dasc_matched_slots(int64_t budget_bytes, int64_t slot_bytes, int64_t *slots);
 
+/* Sec. 4.3, stage 1: a model-load-time permutation of linear-attention head bundles
+ * across the T tensor-parallel ranks that lowers the retained rows of the most loaded
+ * rank (which bounds the number of resident checkpoints).  Applying it to every
+ * coupled weight and state tensor is an exact reindexing.  A bundle is one query/key
+ * head with the H/Hqk value heads that share it; rank r computes bundle positions
+ * [r*Hqk/T, (r+1)*Hqk/T) of every layer.  The paper gives no algorithm; this one
+ * places bundles by retained rows, largest first (ties: lower layer, then lower
+ * bundle), on the least loaded rank (ties: lower rank) that still has room in that
+ * layer, keeps each rank's bundles in their original order, and returns the identity
+ * whenever the result would be no better, so the worst rank never grows.
+ *   unit_count: host int32 [L*H], retained units per (layer, head) as dasc_plan
+ *     returns them (KDA: rows in [0, dk]; GDN: 0 or 1).
+ *   head_perm: host int32 [L*H] out; head_perm[l*H + p] = original head at position p.
+ *   rank_rows, rank_rows_identity: host int64 [T] out; retained rows per rank after
+ *     the permutation and before it.
+ * Errors: DASC_E_INVAL (NULL pointer, n_ranks < 1, Hqk % n_ranks != 0, a count out of
+ * range), DASC_E_SHAPE (bad shape). */
+int dasc_tp_permutation(const dasc_shape *shape, const int32_t *unit_count, int32_t n_ranks,
+                        int32_t *head_perm, int64_t *rank_rows, int64_t *rank_rows_identity);
+
 /* Static message for a status code (never NULL). */
 const char *dasc_strerror(int code);
 

@@ -19,4 +19,5 @@ from .dasc import (  # noqa: F401
     dasc_restore_q8,
     dasc_restore_refresh,
     dasc_static_log_decay,
+    dasc_tp_permutation,
 )

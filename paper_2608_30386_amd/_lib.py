@@ -31,6 +31,7 @@ EXPORTED = (
     "dasc_static_log_decay", "dasc_plan", "dasc_matched_slots", "dasc_strerror",
     "dasc_pack", "dasc_restore", "dasc_pack_q8", "dasc_restore_q8",
     "dasc_refresh_workspace_bytes", "dasc_refresh", "dasc_restore_refresh",
+    "dasc_tp_permutation",
 )
 
 
@@ -88,6 +89,7 @@ def _load() -> C.CDLL:
         "dasc_static_log_decay": [P, P, D, I64, P],
         "dasc_plan": [C.POINTER(PlanDesc), P, C.POINTER(PlanOut)],
         "dasc_matched_slots": [I64, I64, C.POINTER(C.c_int64)],
+        "dasc_tp_permutation": [C.POINTER(Shape), P, I32, P, P, P],
         "dasc_pack": [C.POINTER(Shape), P, I64, P, P, I64, P, I64, P, I32, I64, I32, P],
         "dasc_restore": [C.POINTER(Shape), P, I64, P, I32, I64, I64, P, P, I64, P, I32, P],
         "dasc_pack_q8": [C.POINTER(Shape), P, I64, P, P, I64, P, P, I64, P, I32, P],

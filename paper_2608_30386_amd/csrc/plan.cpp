@@ -220,6 +220,70 @@ extern "C" int dasc_plan(const dasc_plan_desc* desc, const double* g, dasc_plan_
   return DASC_OK;
 }
 
+extern "C" int dasc_tp_permutation(const dasc_shape* shape, const int32_t* unit_count,
+                                   int32_t n_ranks, int32_t* head_perm, int64_t* rank_rows,
+                                   int64_t* rank_rows_identity) {
+  if (!shape) return DASC_E_SHAPE;
+  if (shape->arch != DASC_ARCH_KDA && shape->arch != DASC_ARCH_GDN) return DASC_E_SHAPE;
+  const int L = shape->n_layers, H = shape->n_heads, B = shape->n_qk_heads;
+  if (L <= 0 || H <= 0 || B <= 0 || shape->dk <= 0 || shape->dv <= 0 || H % B != 0)
+    return DASC_E_SHAPE;
+  if (int64_t(L) * H * shape->dk >= (int64_t(1) << 31)) return DASC_E_SHAPE;
+  if (!unit_count || !head_perm || !rank_rows || !rank_rows_identity) return DASC_E_INVAL;
+  if (n_ranks < 1 || B % n_ranks != 0) return DASC_E_INVAL;
+  const bool kda = shape->arch == DASC_ARCH_KDA;
+  const int max_units = kda ? shape->dk : 1;
+  for (int64_t i = 0; i < int64_t(L) * H; ++i)
+    if (unit_count[i] < 0 || unit_count[i] > max_units) return DASC_E_INVAL;
+
+  const int T = n_ranks, g = H / B, cap = B / T;
+  const int64_t rows_per_unit = kda ? 1 : shape->dk;
+  std::vector<int64_t> load(size_t(L) * B, 0);    // retained rows per (layer, bundle)
+  for (int l = 0; l < L; ++l)
+    for (int b = 0; b < B; ++b) {
+      int64_t units = 0;
+      for (int i = 0; i < g; ++i) units += unit_count[int64_t(l) * H + b * g + i];
+      load[size_t(l) * B + b] = units * rows_per_unit;
+    }
+  std::vector<int64_t> ident(T, 0);
+  for (int l = 0; l < L; ++l)
+    for (int b = 0; b < B; ++b) ident[b / cap] += load[size_t(l) * B + b];
+
+  std::vector<int> order(size_t(L) * B);
+  for (size_t i = 0; i < order.size(); ++i) order[i] = int(i);
+  // largest first; ties to the lower (layer, bundle), which is the lower flat index
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int a, int b) { return load[a] > load[b]; });
+  std::vector<int64_t> U(T, 0);
+  std::vector<int> used(size_t(L) * T, 0), owner(size_t(L) * B, 0);
+  for (int item : order) {
+    const int l = item / B;
+    int best = -1;
+    for (int r = 0; r < T; ++r)
+      if (used[size_t(l) * T + r] < cap && (best < 0 || U[r] < U[best])) best = r;
+    owner[item] = best;
+    ++used[size_t(l) * T + best];
+    U[best] += load[item];
+  }
+  if (*std::max_element(U.begin(), U.end()) >= *std::max_element(ident.begin(), ident.end())) {
+    for (int l = 0; l < L; ++l)
+      for (int b = 0; b < B; ++b) owner[size_t(l) * B + b] = b / cap;
+    U = ident;
+  }
+  for (int l = 0; l < L; ++l) {
+    int pos = 0;
+    for (int r = 0; r < T; ++r)
+      for (int b = 0; b < B; ++b)
+        if (owner[size_t(l) * B + b] == r)
+          for (int i = 0; i < g; ++i) head_perm[int64_t(l) * H + pos++] = b * g + i;
+  }
+  for (int r = 0; r < T; ++r) {
+    rank_rows[r] = U[r];
+    rank_rows_identity[r] = ident[r];
+  }
+  return DASC_OK;
+}
+
 extern "C" const char* dasc_strerror(int code) {
   switch (code) {
     case DASC_OK: return "ok";

@@ -112,6 +112,23 @@ def dasc_matched_slots(budget_bytes: int, slot_bytes: int) -> int:
     return out.value
 
 
+def dasc_tp_permutation(shape: Shape, unit_count: np.ndarray, n_ranks: int) -> dict:
+    """Stage-1 head-bundle permutation across TP ranks (host).  unit_count is the plan's
+    [L, H] retained units.  Returns head_perm [L, H], rank_rows [T] and
+    rank_rows_identity [T]."""
+    uc = np.ascontiguousarray(unit_count, dtype=np.int32).reshape(-1)
+    if uc.size != shape.n_layers * shape.n_heads:
+        raise ValueError(f"unit_count has {uc.size} entries, shape needs "
+                         f"{shape.n_layers * shape.n_heads}")
+    perm = np.zeros(uc.size, np.int32)
+    rows = np.zeros(max(n_ranks, 1), np.int64)
+    ident = np.zeros(max(n_ranks, 1), np.int64)
+    _check(LIB.dasc_tp_permutation(C.byref(shape.c()), _ptr(uc), n_ranks, _ptr(perm),
+                                   _ptr(rows), _ptr(ident)), "dasc_tp_permutation")
+    return {"head_perm": perm.reshape(shape.n_layers, shape.n_heads), "rank_rows": rows,
+            "rank_rows_identity": ident}
+
+
 # ---- device calls (torch tensors) ----------------------------------------------------
 
 def _dev(t, dtype, name):

@@ -25,7 +25,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     assert set(names) == set(_lib.EXPORTED)
     lib = C.CDLL(_lib.LIB_PATH)
     for n in names:
@@ -65,6 +65,25 @@ def test_restore_refresh_argument_errors():
     # every argument valid: only dk = dv = 128 has a fused kernel
     assert restore_refresh(kda()) == E.DASC_E_UNSUPPORTED
     assert restore_refresh(kda(dk=128, dv=64)) == E.DASC_E_UNSUPPORTED
+
+
+def test_tp_permutation_argument_errors():
+    E = _lib
+    uc = np.zeros(8, np.int32)
+    out = np.zeros(8, np.int32)
+    r1, r2 = np.zeros(4, np.int64), np.zeros(4, np.int64)
+    ptr = lambda a: a.ctypes.data_as(C.c_void_p)  # noqa: E731
+    call = lambda sh, T, u=uc: LIB.dasc_tp_permutation(  # noqa: E731
+        C.byref(sh) if sh is not None else None, ptr(u), T, ptr(out), ptr(r1), ptr(r2))
+    assert call(None, 2) == E.DASC_E_SHAPE
+    assert call(Shape(E.DASC_ARCH_GDN, 2, 4, 3, 16, 16), 1) == E.DASC_E_SHAPE   # H % Hqk
+    assert call(kda(L=2, H=4), 0) == E.DASC_E_INVAL
+    assert call(kda(L=2, H=4), 3) == E.DASC_E_INVAL                            # Hqk % T
+    assert call(kda(L=2, H=4), 2, np.full(8, 17, np.int32)) == E.DASC_E_INVAL   # > dk
+    assert call(Shape(E.DASC_ARCH_GDN, 2, 4, 2, 16, 16), 2, np.full(8, 2, np.int32)) == E.DASC_E_INVAL
+    assert LIB.dasc_tp_permutation(C.byref(kda(L=2, H=4)), None, 2, ptr(out), ptr(r1),
+                                   ptr(r2)) == E.DASC_E_INVAL
+    assert call(kda(L=2, H=4), 2) == E.DASC_OK
 
 
 def test_strerror_total():

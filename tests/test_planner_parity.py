@@ -77,3 +77,42 @@ def test_matched_slots_paper_budget():
     # App. C.1: 694,681,600 B per rank = 128 dense slots -> 127 deployable
     assert D.dasc_matched_slots(694_681_600, 694_681_600 // 128) == 127
     assert D.dasc_matched_slots(1_236_271_104, 1_236_271_104 // 128) == 127
+
+
+def _compare_perm(sh, unit_count, T):
+    lib = D.dasc_tp_permutation(sh, unit_count, T)
+    orc = OP.tp_permutation(np.asarray(unit_count).reshape(sh.n_layers, sh.n_heads), sh.arch,
+                            sh.n_qk_heads, T, sh.dk)
+    for name in ("head_perm", "rank_rows", "rank_rows_identity"):
+        np.testing.assert_array_equal(lib[name], orc[name], err_msg=name)
+    return lib
+
+
+@pytest.mark.parametrize("name,T", [("kimi_model", 8), ("kimi_model", 4), ("qwen_gdn", 8),
+                                    ("kimi_layer", 8), ("tiny_kda", 2)])
+def test_workload_tp_permutation_bit_exact(name, T):
+    wl = WORKLOADS[name]
+    sh = D.Shape(wl.arch, wl.n_layers, wl.n_heads, wl.n_qk_heads, wl.dk, wl.dv)
+    plan = D.dasc_plan(sh, D.dasc_static_log_decay(log_lambda(wl)), wl.keep_mode, wl.keep_k,
+                       wl.w_max, 1, wl.eps)
+    res = _compare_perm(sh, plan["unit_count"], T)
+    assert res["rank_rows"].sum() == res["rank_rows_identity"].sum() == plan["n_rows"]
+    assert res["rank_rows"].max() <= res["rank_rows_identity"].max()
+
+
+@settings(max_examples=60, deadline=None)
+@given(arch=st.sampled_from(["kda", "gdn"]), L=st.integers(1, 5), B=st.sampled_from([1, 2, 4, 8]),
+       g=st.sampled_from([1, 2, 3]), T=st.sampled_from([1, 2, 4, 8]), dk=st.sampled_from([1, 4, 16]),
+       seed=st.integers(0, 2**31), ties=st.booleans())
+def test_random_tp_permutation_bit_exact(arch, L, B, g, T, dk, seed, ties):
+    if B % T:
+        T = 1
+    rng = np.random.default_rng(seed)
+    H = B * g
+    hi = dk if arch == "kda" else 1
+    uc = rng.integers(0, hi + 1, size=(L, H))
+    if ties:
+        uc = np.full((L, H), hi // 2) + (rng.random((L, H)) < 0.1)
+        uc = np.minimum(uc, hi)
+    sh = D.Shape(arch, L, H, B, dk, 4)
+    _compare_perm(sh, uc, T)
