@@ -117,3 +117,38 @@ def test_rank_sliced_layout_reconcatenates(arch, T):
     back = K.restore(sl, [0, 1], p["unit_row"], np.zeros_like(st), [0, 1], slice_rows=C)
     back_flat = K.restore(flat, [0, 1], p["unit_row"], np.zeros_like(st), [0, 1])
     np.testing.assert_array_equal(back, back_flat)
+
+
+# ---- App. B Scheme 1: the padded layout ------------------------------------------------
+
+@pytest.mark.parametrize("arch,w", [("kda", 64), ("kda", 512), ("gdn", 64)])
+def test_padded_layout_matches_ragged_and_round_trips(arch, w):
+    rng = np.random.default_rng(7)
+    L, H, dk, dv, n = 4, 3, 8, 4, 3
+    p = _plan(arch, L, H, dk, dv, w, seed=5)
+    rpu = p["rows_per_unit"]
+    r_layer = np.diff(p["layer_off"])
+    r_max_rows = int(r_layer.max()) * rpu
+    st = _words(rng, n, L * H * dk, dv)
+    sentinel = np.uint32(0xDEADBEEF)
+    ckpt = np.full((L, n + 1, r_max_rows, dv), sentinel, np.uint32)
+    src, dst = [2, 0, 1], [1, 3, 0]
+    pad = K.pack_padded(st, src, p["unit_row"], p["layer_off"], rpu, ckpt, dst)
+    # the valid entries of each layer are that layer's range of the ragged checkpoint
+    rag = K.pack(st, src, p["unit_row"], np.zeros((1, n + 1, p["n_rows"], dv), np.uint32), dst)
+    for i, d in enumerate(dst):
+        for l in range(L):
+            lo, hi = int(p["layer_off"][l]) * rpu, int(p["layer_off"][l + 1]) * rpu
+            assert np.array_equal(pad[l, d, : hi - lo], rag[0, d, lo:hi])
+            assert np.all(pad[l, d, hi - lo:] == sentinel)           # padding untouched
+    assert np.all(pad[:, 2] == sentinel)                               # unused slot
+    # Load: the same restored state as from the ragged layout (masked source state)
+    back = K.restore_padded(pad, dst, p["unit_row"], p["layer_off"], rpu,
+                            np.zeros((n, L * H * dk, dv), np.uint32), [0, 1, 2])
+    mask = p["inv_row"] >= 0
+    for i in range(n):
+        assert np.array_equal(back[i][mask], st[src[i]][mask])
+        assert np.all(back[i][~mask] == 0)
+    # capacity: padded over ragged rows is the layout gain R_max / r_bar of Eq. 6
+    if p["n_units"]:
+        assert math.isclose(L * r_max_rows / (p["n_rows"]), p["layout_gain"], rel_tol=1e-12)
