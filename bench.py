@@ -361,6 +361,26 @@ def bench_pack_restore_only(torch, args, name):
     tq = {k_: timer.mean_ms(k_) for k_ in ("pack_q8", "restore_q8")}
     bpq = R * n * (dv * 4 + dv + 4)               # read fp32 rows, write int8 rows + scales
     brq = n * (R * (dv + 4) + rows * dv * 4)      # read int8 rows + scales, write fp32 states
+
+    # padded layout (App. B Scheme 1, the comparison layout): same rows moved, L * R_max
+    # rows reserved per checkpoint
+    del q, s
+    off_np, r_max = D.padded_geometry(sh, plan)
+    off = _i32(torch, off_np)
+    ck_pad = torch.empty((sh.n_layers, n, r_max, dv), dtype=torch.float32, device="cuda")
+    for _ in range(args.warmup):
+        D.dasc_pack_padded(sh, states, ids, unit_row, off, ck_pad, ids)
+        D.dasc_restore_padded(sh, ck_pad, ids, off, inv_row, active, ids, n_rows=R)
+    torch.cuda.synchronize()
+    timer.spans.clear()
+    for _ in range(args.steps):
+        timer.run("pack_padded", lambda: D.dasc_pack_padded(sh, states, ids, unit_row, off, ck_pad,
+                                                            ids))
+        timer.run("restore_padded", lambda: D.dasc_restore_padded(sh, ck_pad, ids, off, inv_row,
+                                                                  active, ids, n_rows=R))
+    torch.cuda.synchronize()
+    del ck_pad
+    tp = {k_: timer.mean_ms(k_) for k_ in ("pack_padded", "restore_padded")}
     return {
         "metric": "pack+restore GB/s (full-model KDA checkpoint set)", "value": gbps, "unit": "GB/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
@@ -374,8 +394,10 @@ def bench_pack_restore_only(torch, args, name):
         "kernels": {k_: {"ms": tt[k_], "GBps": b / tt[k_] / 1e6,
                          "hbm_frac": b / tt[k_] / 1e6 / HBM_PEAK_GBPS, "bytes": b}
                     for tt, k_, b in ((t, "pack", bp), (t, "restore", br),
-                                      (tq, "pack_q8", bpq), (tq, "restore_q8", brq))},
+                                      (tq, "pack_q8", bpq), (tq, "restore_q8", brq),
+                                      (tp, "pack_padded", bp), (tp, "restore_padded", br))},
         "q8_checkpoint_bytes": R * (dv + 4), "fp32_checkpoint_bytes": R * dv * 4,
+        "padded_checkpoint_bytes": sh.n_layers * r_max * dv * 4,
         "tp_stage1": tp_stage1(D, sh, plan, T),
         "plan_host_ms": plan_s * 1e3,
     }

@@ -213,6 +213,35 @@ int dasc_restore(const dasc_shape *shape,
                  float *states, int64_t n_pool, const int32_t *dst_slot,
                  int32_t n, dasc_stream_t stream);
 
+/* ---- Padded checkpoints (App. B, Scheme 1: the comparison layout) --------- */
+
+/* Store and Load with the padded layout: every layer reserves r_max_rows rows per
+ * checkpoint (the largest layer's retained rows), ckpt = [L, n_ckpt_slots, r_max_rows,
+ * dv]; entry e < r_l of layer l holds the e-th retained row of that layer, padding is
+ * not written.  Same retained values as the ragged layout; it needs L * r_max_rows
+ * rows per checkpoint instead of n_rows (the layout gain of Eq. 6).
+ *   layer_off_rows: device int32 [L+1], the plan's layer_off times rows per unit
+ *     (1 for KDA, dk for GDN).
+ *   r_max_rows: max over layers of layer_off_rows[l+1] - layer_off_rows[l]; rows a
+ *     layer has past it are not written (pack) and restore as +0.0.
+ *   Other arguments as dasc_pack / dasc_restore (flat addressing, no rank slices).
+ * Errors: as dasc_pack / dasc_restore; DASC_E_INVAL also for r_max_rows < 1 with
+ * n_rows > 0 or r_max_rows >= 2^31. */
+int dasc_pack_padded(const dasc_shape *shape, const float *states, int64_t n_pool,
+                     const int32_t *src_slot, const int32_t *unit_row, int64_t n_rows,
+                     const int32_t *layer_off_rows, int64_t r_max_rows,
+                     float *ckpt, int64_t n_ckpt_slots, const int32_t *dst_slot,
+                     int32_t n, dasc_stream_t stream);
+
+/* For every dense row d of layer l of each destination state:
+ *     states[dst_slot[i]][d][:] = ckpt[l][src_slot[i]][inv_row[d] - layer_off_rows[l]][:]
+ * when inv_row[d] >= 0 (and the entry lies in [0, r_max_rows)), else +0.0. */
+int dasc_restore_padded(const dasc_shape *shape, const float *ckpt, int64_t n_ckpt_slots,
+                        const int32_t *src_slot, const int32_t *layer_off_rows,
+                        int64_t r_max_rows, int64_t n_rows, const int32_t *inv_row,
+                        float *states, int64_t n_pool, const int32_t *dst_slot, int32_t n,
+                        dasc_stream_t stream);
+
 /* ---- INT8 checkpoints (App. E.1, Eq. 10) ---------------------------------- */
 
 /* Pack with symmetric INT8 quantisation.  One scale per (layer, head, key channel),

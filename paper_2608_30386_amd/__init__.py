@@ -11,13 +11,16 @@ from .dasc import (  # noqa: F401
     Shape,
     dasc_matched_slots,
     dasc_pack,
+    dasc_pack_padded,
     dasc_pack_q8,
     dasc_plan,
     dasc_refresh,
     dasc_refresh_workspace_bytes,
     dasc_restore,
+    dasc_restore_padded,
     dasc_restore_q8,
     dasc_restore_refresh,
     dasc_static_log_decay,
     dasc_tp_permutation,
+    padded_geometry,
 )

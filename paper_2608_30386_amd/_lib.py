@@ -31,7 +31,7 @@ EXPORTED = (
     "dasc_static_log_decay", "dasc_plan", "dasc_matched_slots", "dasc_strerror",
     "dasc_pack", "dasc_restore", "dasc_pack_q8", "dasc_restore_q8",
     "dasc_refresh_workspace_bytes", "dasc_refresh", "dasc_restore_refresh",
-    "dasc_tp_permutation",
+    "dasc_tp_permutation", "dasc_pack_padded", "dasc_restore_padded",
 )
 
 
@@ -93,6 +93,8 @@ def _load() -> C.CDLL:
         "dasc_pack": [C.POINTER(Shape), P, I64, P, P, I64, P, I64, P, I32, I64, I32, P],
         "dasc_restore": [C.POINTER(Shape), P, I64, P, I32, I64, I64, P, P, I64, P, I32, P],
         "dasc_pack_q8": [C.POINTER(Shape), P, I64, P, P, I64, P, P, I64, P, I32, P],
+        "dasc_pack_padded": [C.POINTER(Shape), P, I64, P, P, I64, P, I64, P, I64, P, I32, P],
+        "dasc_restore_padded": [C.POINTER(Shape), P, I64, P, P, I64, I64, P, P, I64, P, I32, P],
         "dasc_restore_q8": [C.POINTER(Shape), P, P, I64, P, I64, P, P, I64, P, I32, P],
         "dasc_refresh_workspace_bytes": [C.POINTER(Shape), I32, I32, C.POINTER(C.c_size_t)],
         "dasc_refresh": [C.POINTER(Shape), I32, P, P, I64, P, P, P, P, P, I32, I32, I32, P, SZ, P],

@@ -57,7 +57,8 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(
     const f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
     const int32_t* __restrict__ src_slot, const int32_t* __restrict__ unit_row, int64_t n_rows,
     f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ dst_slot,
-    int64_t slice_rows, int n_ranks, int blocks_per_slice, int rpb, int vpr_rt) {
+    int64_t slice_rows, int n_ranks, int blocks_per_slice, int rpb, int vpr_rt,
+    const int32_t* __restrict__ slice_begin) {
   using G = RowGeom<VPR_LOG2>;
   const int vpr = G::vpr(vpr_rt);
   const int per_ckpt = n_ranks * blocks_per_slice;
@@ -69,8 +70,13 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(
   const int64_t d = dst_slot[i];
   if (s < 0 || s >= n_pool || d < 0 || d >= n_ckpt_slots) return;
   const f32x4* src = states + s * rows_state * vpr;
-  const int64_t slice0 = int64_t(rk) * slice_rows;                 // first packed row of the slice
-  const int64_t slice_end = min(slice0 + slice_rows, n_rows);
+  // Slice rk holds packed rows [slice0, slice_end) at stride slice_rows: equal cuts of
+  // the packed rows (rank slices), or, with slice_begin, the layers of the padded layout
+  // (rows past the stride are not written).
+  const int64_t slice0 = slice_begin ? max(int64_t(slice_begin[rk]), int64_t(0))
+                                     : int64_t(rk) * slice_rows;
+  const int64_t slice_end = min(min(slice_begin ? int64_t(slice_begin[rk + 1]) : n_rows,
+                                    slice0 + slice_rows), n_rows);
   const int64_t row0 = slice0 + int64_t(rb) * rpb;
   // offset of packed row 0 of this slice (may be negative; every row used is >= slice0)
   const int64_t dbase = ((int64_t(rk) * n_ckpt_slots + d) * slice_rows - slice0) * vpr;
@@ -99,12 +105,15 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(
   }
 }
 
-template <int VPR_LOG2>
-__global__ __launch_bounds__(kThreads) void restore_kernel(
+// Restore body; PADDED selects the padded layout, where the slice of a packed row is
+// the layer of its dense row (known per block unless the block straddles two layers).
+template <int VPR_LOG2, bool PADDED>
+__device__ __forceinline__ void restore_body(
     const f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ src_slot,
     int64_t slice_rows, int64_t n_rows, const int32_t* __restrict__ inv_row,
     f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
-    const int32_t* __restrict__ dst_slot, int blocks_per_state, int rpb, int vpr_rt) {
+    const int32_t* __restrict__ dst_slot, int blocks_per_state, int rpb, int vpr_rt,
+    const int32_t* __restrict__ slice_begin, int64_t rows_per_layer) {
   using G = RowGeom<VPR_LOG2>;
   const int vpr = G::vpr(vpr_rt);
   const int i = blockIdx.x / blocks_per_state;
@@ -115,6 +124,12 @@ __global__ __launch_bounds__(kThreads) void restore_kernel(
   f32x4* dst = states + d * rows_state * vpr;
   const int64_t row0 = int64_t(rb) * rpb;
   const int n_vec = rpb * vpr;
+  int64_t blk_layer = -1;   // padded: the layer of every row of this block, if unique
+  if (PADDED) {
+    const int64_t last = min(row0 + rpb, rows_state) - 1;
+    const int64_t l0 = int64_t(uint32_t(row0) / uint32_t(rows_per_layer));
+    if (l0 == int64_t(uint32_t(last) / uint32_t(rows_per_layer))) blk_layer = l0;
+  }
 
   for (int base = 0; base < n_vec; base += kVecPerBlock) {
     f32x4 val[kUnroll];
@@ -129,8 +144,16 @@ __global__ __launch_bounds__(kThreads) void restore_kernel(
         const int c = G::col_of(v, vpr_rt);
         const int64_t p = inv_row[dense];
         if (p >= 0 && p < n_rows) {
-          val[u] = __builtin_nontemporal_load(
-              ckpt + slice_row(p, slice_rows, n_rows, n_ckpt_slots, s) * vpr + c);
+          int64_t row;
+          if (PADDED) {
+            const int64_t l = blk_layer >= 0 ? blk_layer
+                                             : int64_t(uint32_t(dense) / uint32_t(rows_per_layer));
+            const int64_t e = p - slice_begin[l];
+            row = (e >= 0 && e < slice_rows) ? (l * n_ckpt_slots + s) * slice_rows + e : -1;
+          } else {
+            row = slice_row(p, slice_rows, n_rows, n_ckpt_slots, s);
+          }
+          if (row >= 0) val[u] = __builtin_nontemporal_load(ckpt + row * vpr + c);
         }
         dst_off[u] = dense * vpr + c;
       }
@@ -139,6 +162,29 @@ __global__ __launch_bounds__(kThreads) void restore_kernel(
     for (int u = 0; u < kUnroll; ++u)
       if (dst_off[u] >= 0) __builtin_nontemporal_store(val[u], dst + dst_off[u]);
   }
+}
+
+template <int VPR_LOG2>
+__global__ __launch_bounds__(kThreads) void restore_kernel(
+    const f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ src_slot,
+    int64_t slice_rows, int64_t n_rows, const int32_t* __restrict__ inv_row,
+    f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
+    const int32_t* __restrict__ dst_slot, int blocks_per_state, int rpb, int vpr_rt) {
+  restore_body<VPR_LOG2, false>(ckpt, n_ckpt_slots, src_slot, slice_rows, n_rows, inv_row, states,
+                                n_pool, rows_state, dst_slot, blocks_per_state, rpb, vpr_rt,
+                                nullptr, 1);
+}
+
+template <int VPR_LOG2>
+__global__ __launch_bounds__(kThreads) void restore_padded_kernel(
+    const f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ src_slot,
+    int64_t slice_rows, int64_t n_rows, const int32_t* __restrict__ inv_row,
+    f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
+    const int32_t* __restrict__ dst_slot, int blocks_per_state, int rpb, int vpr_rt,
+    const int32_t* __restrict__ slice_begin, int64_t rows_per_layer) {
+  restore_body<VPR_LOG2, true>(ckpt, n_ckpt_slots, src_slot, slice_rows, n_rows, inv_row, states,
+                               n_pool, rows_state, dst_slot, blocks_per_state, rpb, vpr_rt,
+                               slice_begin, rows_per_layer);
 }
 
 int vpr_log2(int vpr) {
@@ -194,7 +240,8 @@ extern "C" int dasc_pack(const dasc_shape* shape, const float* states, int64_t n
                      reinterpret_cast<hipStream_t>(stream),
                      reinterpret_cast<const f32x4*>(states), n_pool, dasc::rows_per_state(shape),
                      src_slot, unit_row, n_rows, reinterpret_cast<f32x4*>(ckpt), n_ckpt_slots,
-                     dst_slot, slice_rows, int(n_ranks), int(bps), rpb, vpr);
+                     dst_slot, slice_rows, int(n_ranks), int(bps), rpb, vpr,
+                     static_cast<const int32_t*>(nullptr));
   return dasc::launch_status();
 }
 
@@ -221,5 +268,67 @@ extern "C" int dasc_restore(const dasc_shape* shape, const float* ckpt, int64_t 
                      reinterpret_cast<const f32x4*>(ckpt), n_ckpt_slots, src_slot, slice_rows,
                      n_rows, inv_row, reinterpret_cast<f32x4*>(states), n_pool, rows, dst_slot,
                      int(bps), rpb, vpr);
+  return dasc::launch_status();
+}
+
+// ---- App. B Scheme 1: padded layout [L, n_slots, r_max_rows, dv] ---------------------
+// The rank-slice kernels with one slice per layer: slice l starts at packed row
+// layer_off_rows[l] and is stored at stride r_max_rows.
+
+extern "C" int dasc_pack_padded(const dasc_shape* shape, const float* states, int64_t n_pool,
+                                const int32_t* src_slot, const int32_t* unit_row,
+                                int64_t n_rows, const int32_t* layer_off_rows,
+                                int64_t r_max_rows, float* ckpt, int64_t n_ckpt_slots,
+                                const int32_t* dst_slot, int32_t n, dasc_stream_t stream) {
+  int rc = check_common(shape, n_pool, n_ckpt_slots, 1, n_rows, n_rows, n);
+  if (rc != DASC_OK) return rc;
+  if (r_max_rows < 0 || r_max_rows > INT32_MAX || (n_rows > 0 && r_max_rows < 1))
+    return DASC_E_INVAL;
+  if (n == 0 || n_rows == 0) return DASC_OK;
+  if (!states || !src_slot || !unit_row || !layer_off_rows || !ckpt || !dst_slot)
+    return DASC_E_INVAL;
+  if (!dasc::aligned16(states) || !dasc::aligned16(ckpt)) return DASC_E_INVAL;
+  const int L = shape->n_layers;
+  const int vpr = shape->dv / 4;
+  const int rpb = rows_per_block(vpr);
+  const int64_t bps = (std::min<int64_t>(r_max_rows, n_rows) + rpb - 1) / rpb;
+  const int64_t blocks = bps * L * n;
+  if (blocks > INT32_MAX) return DASC_E_INVAL;
+  (void)hipGetLastError();
+  DASC_LAUNCH_BY_VPR(pack_kernel, vpr_log2(vpr), dim3(unsigned(blocks)),
+                     reinterpret_cast<hipStream_t>(stream),
+                     reinterpret_cast<const f32x4*>(states), n_pool, dasc::rows_per_state(shape),
+                     src_slot, unit_row, n_rows, reinterpret_cast<f32x4*>(ckpt), n_ckpt_slots,
+                     dst_slot, r_max_rows, L, int(bps), rpb, vpr, layer_off_rows);
+  return dasc::launch_status();
+}
+
+extern "C" int dasc_restore_padded(const dasc_shape* shape, const float* ckpt,
+                                   int64_t n_ckpt_slots, const int32_t* src_slot,
+                                   const int32_t* layer_off_rows, int64_t r_max_rows,
+                                   int64_t n_rows, const int32_t* inv_row, float* states,
+                                   int64_t n_pool, const int32_t* dst_slot, int32_t n,
+                                   dasc_stream_t stream) {
+  int rc = check_common(shape, n_pool, n_ckpt_slots, 1, n_rows, n_rows, n);
+  if (rc != DASC_OK) return rc;
+  if (r_max_rows < 0 || r_max_rows > INT32_MAX || (n_rows > 0 && r_max_rows < 1))
+    return DASC_E_INVAL;
+  if (n == 0) return DASC_OK;
+  if (!src_slot || !inv_row || !states || !dst_slot) return DASC_E_INVAL;
+  if (n_rows > 0 && (!ckpt || !layer_off_rows)) return DASC_E_INVAL;
+  if (!dasc::aligned16(states) || !dasc::aligned16(ckpt)) return DASC_E_INVAL;
+  if (n_rows == 0) r_max_rows = 1;  // nothing is read
+  const int vpr = shape->dv / 4;
+  const int rpb = rows_per_block(vpr);
+  const int64_t rows = dasc::rows_per_state(shape);
+  const int64_t bps = (rows + rpb - 1) / rpb;
+  if (bps * n > INT32_MAX) return DASC_E_INVAL;
+  (void)hipGetLastError();
+  DASC_LAUNCH_BY_VPR(restore_padded_kernel, vpr_log2(vpr), dim3(unsigned(bps * n)),
+                     reinterpret_cast<hipStream_t>(stream),
+                     reinterpret_cast<const f32x4*>(ckpt), n_ckpt_slots, src_slot, r_max_rows,
+                     n_rows, inv_row, reinterpret_cast<f32x4*>(states), n_pool, rows, dst_slot,
+                     int(bps), rpb, vpr, n_rows > 0 ? layer_off_rows : nullptr,
+                     int64_t(shape->n_heads) * shape->dk);
   return dasc::launch_status();
 }

@@ -192,6 +192,52 @@ def dasc_restore(shape: Shape, ckpt, src_slot, inv_row, states, dst_slot, n_rows
         _stream(stream)), "dasc_restore")
 
 
+def padded_geometry(shape: Shape, plan: dict) -> tuple[np.ndarray, int]:
+    """(layer_off_rows [L+1] int32, r_max_rows) of the padded layout for a plan."""
+    rpu = int(plan["rows_per_unit"])
+    off = (np.asarray(plan["layer_off"], dtype=np.int64) * rpu).astype(np.int32)
+    return off, int(np.diff(off).max()) if off.size > 1 else 0
+
+
+def dasc_pack_padded(shape: Shape, states, src_slot, unit_row, layer_off_rows, ckpt, dst_slot,
+                     stream=None) -> None:
+    """App. B Scheme 1 pack; ckpt is [L, n_slots, r_max_rows, dv] float32."""
+    import torch
+
+    L, n_slots, r_max = ckpt.shape[0], ckpt.shape[1], ckpt.shape[2]
+    if L != shape.n_layers or ckpt.dim() != 4:
+        raise ValueError("padded ckpt must be [L, n_slots, r_max_rows, dv]")
+    _need(states, states.shape[0] * shape.rows * shape.dv, "states")
+    _need(layer_off_rows, L + 1, "layer_off_rows")
+    _need(dst_slot, src_slot.numel(), "dst_slot")
+    _check(LIB.dasc_pack_padded(
+        C.byref(shape.c()), _dev(states, torch.float32, "states"), states.shape[0],
+        _dev(src_slot, torch.int32, "src_slot"), _dev(unit_row, torch.int32, "unit_row"),
+        unit_row.numel(), _dev(layer_off_rows, torch.int32, "layer_off_rows"), r_max,
+        _dev(ckpt, torch.float32, "ckpt"), n_slots, _dev(dst_slot, torch.int32, "dst_slot"),
+        src_slot.numel(), _stream(stream)), "dasc_pack_padded")
+
+
+def dasc_restore_padded(shape: Shape, ckpt, src_slot, layer_off_rows, inv_row, states, dst_slot,
+                        n_rows: int, stream=None) -> None:
+    """App. B Scheme 1 restore from ckpt [L, n_slots, r_max_rows, dv]."""
+    import torch
+
+    L, n_slots, r_max = ckpt.shape[0], ckpt.shape[1], ckpt.shape[2]
+    if L != shape.n_layers or ckpt.dim() != 4:
+        raise ValueError("padded ckpt must be [L, n_slots, r_max_rows, dv]")
+    _need(states, states.shape[0] * shape.rows * shape.dv, "states")
+    _need(layer_off_rows, L + 1, "layer_off_rows")
+    _need(inv_row, shape.rows, "inv_row")
+    _need(dst_slot, src_slot.numel(), "dst_slot")
+    _check(LIB.dasc_restore_padded(
+        C.byref(shape.c()), _dev(ckpt, torch.float32, "ckpt"), n_slots,
+        _dev(src_slot, torch.int32, "src_slot"), _dev(layer_off_rows, torch.int32, "layer_off_rows"),
+        r_max, n_rows, _dev(inv_row, torch.int32, "inv_row"), _dev(states, torch.float32, "states"),
+        states.shape[0], _dev(dst_slot, torch.int32, "dst_slot"), src_slot.numel(),
+        _stream(stream)), "dasc_restore_padded")
+
+
 def dasc_pack_q8(shape: Shape, states, src_slot, unit_row, q, scale, dst_slot, stream=None) -> None:
     """INT8 pack: q [n_slots, R, dv] int8, scale [n_slots, R] float32 (see dasc.h)."""
     import torch

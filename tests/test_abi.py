@@ -25,7 +25,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 14
     assert set(names) == set(_lib.EXPORTED)
     lib = C.CDLL(_lib.LIB_PATH)
     for n in names:
@@ -84,6 +84,42 @@ def test_tp_permutation_argument_errors():
     assert LIB.dasc_tp_permutation(C.byref(kda(L=2, H=4)), None, 2, ptr(out), ptr(r1),
                                    ptr(r2)) == E.DASC_E_INVAL
     assert call(kda(L=2, H=4), 2) == E.DASC_OK
+
+
+def test_padded_argument_errors():
+    E = _lib
+    sh = kda()
+
+    def pp(shape=sh, n=1, r_max=4, n_rows=4, ptrs=None, n_pool=1, n_slots=1):
+        p = dict(states=FAKE, src=FAKE, unit=FAKE, off=FAKE, ckpt=FAKE, dst=FAKE)
+        p.update(ptrs or {})
+        return LIB.dasc_pack_padded(C.byref(shape) if shape is not None else None, p["states"],
+                                    n_pool, p["src"], p["unit"], n_rows, p["off"], r_max,
+                                    p["ckpt"], n_slots, p["dst"], n, None)
+
+    def rp(shape=sh, n=1, r_max=4, n_rows=4, ptrs=None, n_pool=1, n_slots=1):
+        p = dict(ckpt=FAKE, src=FAKE, off=FAKE, inv=FAKE, states=FAKE, dst=FAKE)
+        p.update(ptrs or {})
+        return LIB.dasc_restore_padded(C.byref(shape) if shape is not None else None, p["ckpt"],
+                                       n_slots, p["src"], p["off"], r_max, n_rows, p["inv"],
+                                       p["states"], n_pool, p["dst"], n, None)
+
+    for f in (pp, rp):
+        assert f(shape=None) == E.DASC_E_SHAPE
+        assert f(shape=kda(dv=6)) == E.DASC_E_SHAPE
+        assert f(n=-1) == E.DASC_E_INVAL
+        assert f(r_max=0) == E.DASC_E_INVAL
+        assert f(r_max=1 << 31) == E.DASC_E_INVAL
+        assert f(n_pool=0) == E.DASC_E_INVAL
+        assert f(n_slots=0) == E.DASC_E_INVAL
+        assert f(n_rows=10**6) == E.DASC_E_SHAPE
+        assert f(n=0) == E.DASC_OK                                     # nothing to do
+    for name in ("states", "src", "unit", "off", "ckpt", "dst"):
+        assert pp(ptrs={name: None}) == E.DASC_E_INVAL, name
+    for name in ("ckpt", "src", "off", "inv", "states", "dst"):
+        assert rp(ptrs={name: None}) == E.DASC_E_INVAL, name
+    assert pp(ptrs={"ckpt": FAKE_ODD}) == E.DASC_E_INVAL
+    assert rp(ptrs={"states": FAKE_ODD}) == E.DASC_E_INVAL
 
 
 def test_strerror_total():

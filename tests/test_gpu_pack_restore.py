@@ -160,3 +160,61 @@ def test_out_of_range_device_indices_are_skipped():
     assert torch.equal(h[0, 2], torch.full_like(h[0, 2], 9.0))     # bad destination slot: skipped
     assert torch.equal(h[0, 0, 0], torch.full_like(h[0, 0, 0], 9.0))  # bad row: not written
     assert torch.equal(h[0, 0, 1:], st[0].reshape(-1, sh.dv)[unit_row[1:]].cpu())
+
+
+# ---- App. B Scheme 1: the padded layout ------------------------------------------------
+
+def _padded_roundtrip(sh, plan, states_np, src, dst, n_slots):
+    import torch
+
+    n_pool, rows, dv, L = states_np.shape[0], sh.rows, sh.dv, sh.n_layers
+    R = int(plan["n_rows"])
+    off, r_max = D.padded_geometry(sh, plan)
+    rpu = int(plan["rows_per_unit"])
+    words = states_np.reshape(n_pool, rows, dv).view(np.uint32)
+    st = dev(states_np.reshape(n_pool, L, sh.n_heads, sh.dk, dv))
+    sentinel = np.full((L, n_slots, max(r_max, 1), dv), 0x5A5A5A5A, dtype=np.uint32)
+    ck = dev(sentinel.view(np.float32).copy())
+    announce(f"pack_padded {sh} R={R} r_max_rows={r_max} n={len(src)}")
+    D.dasc_pack_padded(sh, st, dev_i32(src), dev_i32(plan["unit_row"]), dev_i32(off), ck,
+                       dev_i32(dst))
+    torch.cuda.synchronize()
+    want = OK.pack_padded(words, src, plan["unit_row"], plan["layer_off"], rpu, sentinel, dst)
+    assert np.array_equal(host_words(ck), want), "padded pack differs from the oracle"
+    garbage = np.full((n_pool, rows, dv), 0x3C3C3C3C, dtype=np.uint32)
+    out = dev(garbage.view(np.float32).reshape(n_pool, L, sh.n_heads, sh.dk, dv).copy())
+    back = list(range(len(dst)))[::-1]
+    announce(f"restore_padded {sh} R={R} n={len(dst)}")
+    D.dasc_restore_padded(sh, ck, dev_i32(dst), dev_i32(off), dev_i32(plan["inv_row"]), out,
+                          dev_i32(back), n_rows=R)
+    torch.cuda.synchronize()
+    want_r = OK.restore_padded(want, dst, plan["unit_row"], plan["layer_off"], rpu, garbage, back)
+    assert np.array_equal(host_words(out).reshape(n_pool, rows, dv), want_r), \
+        "padded restore differs from the oracle"
+    return L * r_max, R
+
+
+def test_padded_layout_full_model_kda():
+    wl = WORKLOADS["kimi_model"]
+    lib, _ = plans(wl)
+    sh = shape_of(wl)
+    st = states_host(wl, 4)
+    padded_rows, R = _padded_roundtrip(sh, lib, st, src=[3, 1, 0, 2], dst=[2, 0, 4, 1], n_slots=5)
+    announce(f"kimi_model padded rows {padded_rows} vs ragged {R}: gain {padded_rows / R:.2f}")
+    assert math.isclose(padded_rows / R, lib["layout_gain"], rel_tol=1e-12)
+
+
+def test_padded_layout_gdn_and_uneven_layers():
+    wl = WORKLOADS["qwen_gdn"]
+    lib, _ = plans(wl)
+    _padded_roundtrip(shape_of(wl), lib, states_host(wl, 2), src=[1, 0], dst=[0, 1], n_slots=2)
+    rng = np.random.default_rng(9)
+    L, H, dk, dv = 5, 3, 16, 20                      # ragged row width, an empty layer
+    sh = D.Shape("kda", L, H, H, dk, dv)
+    g = D.dasc_static_log_decay(rng.uniform(math.log(1e-4), 0, size=(L, H, dk)))
+    g[2] = math.log(1e-3) / 1.0                       # layer 2: nothing kept
+    g[4, 0] = math.log(1e-3) / 1e4                    # layer 4, head 0: everything kept
+    plan = D.dasc_plan(sh, g, "threshold", 0, 64)
+    st = _plant((0.1 * rng.standard_normal((3, L, H, dk, dv))).astype(np.float32).view(np.uint32),
+                rng).view(np.float32)
+    _padded_roundtrip(sh, plan, st, src=[2, 0, 1], dst=[1, 2, 0], n_slots=4)
