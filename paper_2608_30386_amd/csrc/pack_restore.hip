@@ -53,7 +53,7 @@ inline int rows_per_block(int vpr) { return vpr >= kVecPerBlock ? 1 : kVecPerBlo
 // A block owns a tile of rows of one rank slice of one checkpoint, so the slice of a
 // packed row is known per block and the destination needs no per-row division.
 template <int VPR_LOG2>
-__global__ __launch_bounds__(kThreads) void pack_kernel(
+__device__ __forceinline__ void pack_body(
     const f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
     const int32_t* __restrict__ src_slot, const int32_t* __restrict__ unit_row, int64_t n_rows,
     f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ dst_slot,
@@ -107,6 +107,27 @@ __global__ __launch_bounds__(kThreads) void pack_kernel(
 
 // Restore body; PADDED selects the padded layout, where the slice of a packed row is
 // the layer of its dense row (known per block unless the block straddles two layers).
+template <int VPR_LOG2>
+__global__ __launch_bounds__(kThreads) void pack_kernel(
+    const f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
+    const int32_t* __restrict__ src_slot, const int32_t* __restrict__ unit_row, int64_t n_rows,
+    f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ dst_slot,
+    int64_t slice_rows, int n_ranks, int blocks_per_slice, int rpb, int vpr_rt) {
+  pack_body<VPR_LOG2>(states, n_pool, rows_state, src_slot, unit_row, n_rows, ckpt, n_ckpt_slots,
+                      dst_slot, slice_rows, n_ranks, blocks_per_slice, rpb, vpr_rt, nullptr);
+}
+
+template <int VPR_LOG2>
+__global__ __launch_bounds__(kThreads) void pack_padded_kernel(
+    const f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
+    const int32_t* __restrict__ src_slot, const int32_t* __restrict__ unit_row, int64_t n_rows,
+    f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ dst_slot,
+    int64_t slice_rows, int n_ranks, int blocks_per_slice, int rpb, int vpr_rt,
+    const int32_t* __restrict__ slice_begin) {
+  pack_body<VPR_LOG2>(states, n_pool, rows_state, src_slot, unit_row, n_rows, ckpt, n_ckpt_slots,
+                      dst_slot, slice_rows, n_ranks, blocks_per_slice, rpb, vpr_rt, slice_begin);
+}
+
 template <int VPR_LOG2, bool PADDED>
 __device__ __forceinline__ void restore_body(
     const f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ src_slot,
@@ -240,8 +261,7 @@ extern "C" int dasc_pack(const dasc_shape* shape, const float* states, int64_t n
                      reinterpret_cast<hipStream_t>(stream),
                      reinterpret_cast<const f32x4*>(states), n_pool, dasc::rows_per_state(shape),
                      src_slot, unit_row, n_rows, reinterpret_cast<f32x4*>(ckpt), n_ckpt_slots,
-                     dst_slot, slice_rows, int(n_ranks), int(bps), rpb, vpr,
-                     static_cast<const int32_t*>(nullptr));
+                     dst_slot, slice_rows, int(n_ranks), int(bps), rpb, vpr);
   return dasc::launch_status();
 }
 
@@ -295,7 +315,7 @@ extern "C" int dasc_pack_padded(const dasc_shape* shape, const float* states, in
   const int64_t blocks = bps * L * n;
   if (blocks > INT32_MAX) return DASC_E_INVAL;
   (void)hipGetLastError();
-  DASC_LAUNCH_BY_VPR(pack_kernel, vpr_log2(vpr), dim3(unsigned(blocks)),
+  DASC_LAUNCH_BY_VPR(pack_padded_kernel, vpr_log2(vpr), dim3(unsigned(blocks)),
                      reinterpret_cast<hipStream_t>(stream),
                      reinterpret_cast<const f32x4*>(states), n_pool, dasc::rows_per_state(shape),
                      src_slot, unit_row, n_rows, reinterpret_cast<f32x4*>(ckpt), n_ckpt_slots,
