@@ -33,7 +33,6 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 matrix peak
-FP32_VALU_PEAK_TFLOPS = 78.6    # 256 CU x 64 FMA lanes/clk x 2 FLOP x 2.4 GHz (no packed FP32)
 # Chunked WY form at 32-token chunks, dk = dv = 128, per head-token: the three 16x16
 # A tiles (3*16*16*128 MAC), K_G S (32*128*128), T'(V - K_G S) (32*32*128)
 # and K_H^T U (128*32*128), per 32 tokens, 2 FLOP per MAC.
@@ -459,9 +458,11 @@ def bench_gdn(torch, args):
     bp, br = 2 * R * dv * 4 * n, (R + rows) * dv * 4 * n
     om_heads = int((plan["inv_row"].reshape(-1, sh.dk) < 0).all(axis=1).sum())
     heads = wl.n_req * om_heads
-    per_head = 2 * W * sh.dk + 2 * W * dv + 4 * W + 4 * W + 4 * sh.dk * dv   # k, v, g, beta, write
+    # per refreshed head: k, v (bf16), g, beta (fp32), the restored head read and written
+    per_head = 2 * W * sh.dk + 2 * W * dv + 4 * W + 4 * W + 2 * 4 * sh.dk * dv
+    bytes_ref = heads * per_head
+    ach = bytes_ref / (t["refresh_all_layers"] / 1e3) / 1e9          # GB/s
     flops = 5.0 * sh.dk * dv * W * heads
-    ach = flops / (t["refresh_all_layers"] / 1e3) / 1e12
     return {
         "metric": "GDN pack/restore GB/s + refresh tokens/s (36 layers)",
         "value": wl.n_req * W / (t["refresh_all_layers"] / 1e3), "unit": "tokens/s (all 36 layers)",
@@ -471,13 +472,15 @@ def bench_gdn(torch, args):
         "config": {"workload": f"Qwen-GDN 36 layers 16 qk / 32 v heads 128x128: pack+restore {n} "
                                f"checkpoints (12 of 32 heads kept), refresh {wl.n_req} requests x "
                                f"{om_heads} omitted heads W={W}"},
-        "roofline": {"bound": "alu", "achieved": ach, "peak": FP32_VALU_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": ach / FP32_VALU_PEAK_TFLOPS, "traffic": None,
-                     "kernel": "refresh"},
+        "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": ach / HBM_PEAK_GBPS, "traffic": None, "kernel": "refresh",
+                     "work_per_launch": f"{bytes_ref // wl.n_layers} B per layer launch "
+                                        f"({heads // wl.n_layers} heads)",
+                     "recurrence_TFLOPs": flops / (t["refresh_all_layers"] / 1e3) / 1e12},
         "kernels": {"pack": {"ms": t["pack"], "GBps": bp / t["pack"] / 1e6},
                     "restore": {"ms": t["restore"], "GBps": br / t["restore"] / 1e6},
-                    "refresh_all_layers": {"ms": t["refresh_all_layers"],
-                                           "GBps": heads * per_head / t["refresh_all_layers"] / 1e6}},
+                    "refresh_all_layers": {"ms": t["refresh_all_layers"], "GBps": ach,
+                                           "launches": wl.n_layers, "bytes": bytes_ref}},
         "plan_host_ms": plan_s * 1e3,
     }
 
