@@ -56,7 +56,8 @@ def parse():
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("pack_restore.hip", "quant.hip", "refresh.hip", "refresh_wy.hip", "ckpt_layout.h",
+    for f in ("pack_restore.hip", "quant.hip", "refresh.hip", "refresh_wy.hip", "refresh_wy_gdn.hip",
+              "ckpt_layout.h",
               "refresh_kernels.h", "launch_common.h"):
         with open(os.path.join(ROOT, "paper_2608_30386_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())

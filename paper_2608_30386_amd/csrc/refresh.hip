@@ -143,7 +143,7 @@ extern "C" int dasc_refresh(const dasc_shape* shape, int32_t layer, const int32_
   if (workspace_bytes < need || (need > 0 && !workspace)) return DASC_E_WORKSPACE;
   const int dk = shape->dk, dv = shape->dv;
   if (dv > 256) return DASC_E_UNSUPPORTED;
-  if (int64_t(n_req) * shape->n_heads > INT32_MAX) return DASC_E_INVAL;
+  if (2 * int64_t(n_req) * shape->n_heads > INT32_MAX) return DASC_E_INVAL;  // GDN: 2 blocks a head
 
   const bool per_channel = shape->arch == DASC_ARCH_KDA;
   const int threads = ((dv + 63) / 64) * 64;
@@ -153,9 +153,18 @@ extern "C" int dasc_refresh(const dasc_shape* shape, int32_t layer, const int32_
   const int zero = init_mode == DASC_INIT_ZERO;
   (void)hipGetLastError();
   // The chunked MFMA kernel serves dk = dv = 128; every other shape, or an explicit
-  // DASC_REFRESH_KERNEL=column, takes the per-column fp32 kernel.
+  // DASC_REFRESH_KERNEL=column, takes the per-column fp32 kernel.  GDN heads at that
+  // shape take the scalar-gate kernel unless DASC_REFRESH_KERNEL=wy asks for the
+  // channel-wise one (both exist for comparison).
   const char* pick = std::getenv("DASC_REFRESH_KERNEL");
   const bool force_column = pick && std::strcmp(pick, "column") == 0;
+  const bool force_wy = pick && std::strcmp(pick, "wy") == 0;
+  if (!force_column && !force_wy && !per_channel && dasc::refresh_wy_supported(dk, dv)) {
+    dasc::launch_refresh_wy_gdn(n_req, shape->n_heads, shape->n_qk_heads, layer,
+                                shape->n_layers, inv_row, states, n_pool, slot, k, v, g, beta, W,
+                                zero, st);
+    return dasc::launch_status();
+  }
   if (!force_column && dasc::refresh_wy_supported(dk, dv)) {
     dasc::launch_refresh_wy(per_channel, n_req, shape->n_heads, shape->n_qk_heads, layer,
                             shape->n_layers, inv_row, states, n_pool, slot, k, v, g, beta, W,

@@ -14,6 +14,13 @@ void launch_refresh_wy(bool per_channel, int n_req, int H, int Hqk, int layer, i
                        const uint16_t* k, const uint16_t* v, const float* g, const float* beta,
                        int W, int init_zero, hipStream_t st);
 
+// GDN heads (scalar gate per token), dk = dv = 128: keys enter the MFMAs exactly and
+// the decays stay outside the contractions; two blocks per head (value-column halves).
+void launch_refresh_wy_gdn(int n_req, int H, int Hqk, int layer, int L, const int32_t* inv_row,
+                           float* states, int64_t n_pool, const int32_t* slot, const uint16_t* k,
+                           const uint16_t* v, const float* g, const float* beta, int W,
+                           int init_zero, hipStream_t st);
+
 // The same kernel fused with the restore of the layer: the initial state of each head is
 // read from the packed checkpoint (kept rows; omitted rows start at zero) and every row
 // of the layer is written (omitted rows refreshed, kept rows copied bit for bit).

@@ -217,3 +217,26 @@ def test_chunked_and_column_kernels_agree(monkeypatch):
     announce(f"chunked vs column max diff / max {diff / scale:.2e}")
     assert diff <= 1e-3 * scale
     assert np.array_equal(a.reshape(n_req, -1, 128)[:, ~om], b.reshape(n_req, -1, 128)[:, ~om])
+
+
+def test_gdn_scalar_gate_kernel_matches_channel_kernel(monkeypatch):
+    # GDN heads take the scalar-gate kernel; the channel-wise kernel must give the same
+    # state to within both kernels' distance from the oracle, and both stay in the bar
+    wl = WORKLOADS["qwen_gdn"]
+    lib, _ = plans(wl)
+    sh = shape_of(wl)
+    n_req, layer, W = 3, 5, 333
+    pool = restored_states(wl, lib, n_req)
+    inp = refresh_inputs(wl, W, log_lambda(wl)[layer], n_req=n_req, salt=layer)
+    a = run_refresh(sh, pool, layer, lib["inv_row"], inp, W)
+    monkeypatch.setenv("DASC_REFRESH_KERNEL", "wy")
+    b = run_refresh(sh, pool, layer, lib["inv_row"], inp, W)
+    lo = layer * sh.n_heads * sh.dk
+    om = (lib["inv_row"][lo:lo + sh.n_heads * sh.dk] < 0).reshape(sh.n_heads, sh.dk)
+    pairs = sample_pairs(n_req, sh.n_heads, om, 6, seed=1)
+    for got in (a, b):
+        check(sh, pool, got, layer, lib["inv_row"], inp, pairs)
+    diff = np.abs(a[:, layer][:, om] - b[:, layer][:, om]).max()
+    scale = np.abs(b[:, layer][:, om]).max()
+    announce(f"gdn scalar-gate vs channel kernel max diff / max {diff / scale:.2e}")
+    assert diff <= 1e-4 * scale
