@@ -17,12 +17,17 @@
 // S-independent part (A, T, T') is recomputed by both halves; it is cheap here, and the
 // split doubles the blocks of a launch (a layer of a GDN model has few omitted heads).
 //
-// Per chunk: stage (keys row-major and transposed, this half's values transposed, gates
-// and beta; the running sum of the gates on wave 0) | A tiles on waves 0-2 and X on
-// every wave | T = (I + A)^{-1} diagonal blocks on wave 0 | T' (T10 on wave 1) | U and
-// the state update.  Register chaining, operand splitting, padded LDS rows and the
-// buffer-resource loads (tokens past the window read as zeros: identity steps) are as
-// in the channel-wise kernel; per-token log-gates are floored at -10 in the same way.
+// Software pipeline over chunks (two LDS buffers for a chunk's keys, values, gates and
+// A): with b = n mod 2,
+//   P1  wave 0 inverts the diagonal blocks of I + A(n); waves 1-3 form X(n) on their
+//       columns and stage chunk n+1 into buffer b^1 (wave 1 also sums its gates);
+//   P2  wave 0 forms X(n); wave 1 forms T10(n) and T'(n); waves 2-3 write the rest of
+//       T'(n) and the A tiles of chunk n+1; waves 1-3 issue the loads of chunk n+2;
+//   P3  every wave forms U(n) and updates its columns of S'.
+// Three barriers a chunk; the serial inversion runs beside the staging and X.  Register
+// chaining, operand splitting, padded LDS rows and the buffer-resource loads (tokens
+// past the window read as zeros: identity steps) are as in the channel-wise kernel;
+// per-token log-gates are floored at -10 in the same way.
 
 #include <hip/hip_runtime.h>
 
@@ -48,18 +53,21 @@ constexpr int SK = 136;     // bf16 [C][SK]   keys, row-major
 constexpr int SV = 40;      // bf16 [D][SV]   keys transposed; [DH][SV] values transposed
 constexpr int SP = 36;      // bf16 [C][SP]   T'
 
-constexpr int OFF_K = 0;                        // bf16 [C][SK]
-constexpr int OFF_KT = OFF_K + C * SK * 2;      // bf16 [D][SV]
-constexpr int OFF_VT = OFF_KT + D * SV * 2;     // bf16 [DH][SV]
-constexpr int OFF_A = OFF_VT + DH * SV * 2;     // f32  [C][C]
-constexpr int OFF_T = OFF_A + C * C * 4;        // f32  [C][C]
+// LDS map (bytes): one buffer per chunk parity, then T and T' (single).
+constexpr int B_K = 0;                          // bf16 [C][SK]  keys
+constexpr int B_KT = B_K + C * SK * 2;          // bf16 [D][SV]  keys transposed
+constexpr int B_VT = B_KT + D * SV * 2;         // bf16 [DH][SV] this half's values transposed
+constexpr int B_A = B_VT + DH * SV * 2;         // f32  [C][C]   A
+constexpr int B_G = B_A + C * C * 4;            // f32  [C] G_t
+constexpr int B_EG = B_G + C * 4;               // f32  [C] 2^{G_t}
+constexpr int B_EH = B_EG + C * 4;              // f32  [C] 2^{G_C - G_t}
+constexpr int B_BETA = B_EH + C * 4;            // f32  [C]
+constexpr int BUF = B_BETA + C * 4;
+constexpr int OFF_T = 2 * BUF;                  // f32  [C][C]
 constexpr int OFF_TPH = OFF_T + C * C * 4;      // bf16 [C][SP]
 constexpr int OFF_TPL = OFF_TPH + C * SP * 2;
-constexpr int OFF_G = OFF_TPL + C * SP * 2;     // f32  [C] G_t
-constexpr int OFF_EG = OFF_G + C * 4;           // f32  [C] 2^{G_t}
-constexpr int OFF_EH = OFF_EG + C * 4;          // f32  [C] 2^{G_C - G_t}
-constexpr int OFF_BETA = OFF_EH + C * 4;        // f32  [C]
-constexpr int LDS_BYTES = OFF_BETA + C * 4;
+constexpr int LDS_BYTES = OFF_TPL + C * SP * 2;
+static_assert(BUF % 16 == 0 && LDS_BYTES <= 81920, "two blocks per CU");
 
 __device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -113,17 +121,17 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, const float* __restrict__ g,
     const float* __restrict__ beta, int W, int init_zero) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
-  uint16_t* sK = reinterpret_cast<uint16_t*>(smem + OFF_K);
-  uint16_t* sKT = reinterpret_cast<uint16_t*>(smem + OFF_KT);
-  uint16_t* sVT = reinterpret_cast<uint16_t*>(smem + OFF_VT);
-  float* sA = reinterpret_cast<float*>(smem + OFF_A);
   float* sT = reinterpret_cast<float*>(smem + OFF_T);
   __bf16* sTPH = reinterpret_cast<__bf16*>(smem + OFF_TPH);
   __bf16* sTPL = reinterpret_cast<__bf16*>(smem + OFF_TPL);
-  float* sG = reinterpret_cast<float*>(smem + OFF_G);
-  float* sEG = reinterpret_cast<float*>(smem + OFF_EG);
-  float* sEH = reinterpret_cast<float*>(smem + OFF_EH);
-  float* sBeta = reinterpret_cast<float*>(smem + OFF_BETA);
+  auto bK = [&](int b) { return reinterpret_cast<uint16_t*>(smem + b * BUF + B_K); };
+  auto bKT = [&](int b) { return reinterpret_cast<uint16_t*>(smem + b * BUF + B_KT); };
+  auto bVT = [&](int b) { return reinterpret_cast<uint16_t*>(smem + b * BUF + B_VT); };
+  auto bA = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_A); };
+  auto bG = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_G); };
+  auto bEG = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_EG); };
+  auto bEH = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_EH); };
+  auto bBeta = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_BETA); };
 
   const int half = blockIdx.x & 1;
   const int nh = blockIdx.x >> 1;
@@ -158,60 +166,72 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
   const __amdgpu_buffer_rsrc_t rk = rsrc(kp, W * D * 2), rv = rsrc(vp, W * D * 2);
   const __amdgpu_buffer_rsrc_t rg = rsrc(gp, W * 4), rb = rsrc(bp, W * 4);
 
-  // Load ownership (issued one chunk ahead):
-  //   keys row-major: two 8-channel units (token kt, channels kc8..) per thread;
-  //   keys transposed: channels 2p, 2p + 1 of tokens 8o .. 8o+7 (p = tid % 64, o = tid / 64);
-  //   values: columns 64 half + 2p', +1 of tokens 4o' .. 4o'+3 (p' = tid % 32, o' = tid / 32);
-  //   gate and beta: token tid (threads below 32).
-  const int kp2 = tid & 63, ko = tid >> 6;
-  const int vp2 = tid & 31, vo = tid >> 5;
-  uint4 kraw[2];
-  uint32_t kw[8], vw[4];
-  float graw, braw;
+  // Waves 1-3 (192 threads, index st = tid - 64) load and stage a chunk:
+  //   keys row-major: 8-channel units u = st + 192 i (< 512): token u / 16, channels 8 (u % 16);
+  //   keys transposed: items p = st + 192 i (< 256): channels 2 (p % 64), +1, tokens 8 (p / 64) .. +7;
+  //   values: items p (< 256): columns 64 half + 2 (p % 32), +1, tokens 4 (p / 32) .. +3;
+  //   gate and beta: token st % 32 (wave 1 sums them).
+  const int st = tid - 64;
+  uint4 kraw[3];
+  uint32_t kw[2][8], vw[2][4];
+  float graw = 0.f, braw = 0.f;
   auto fetch = [&](int c0) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
-      kraw[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, (t * D + c8) * 2, c0 * D * 2, 0));
+    for (int i = 0; i < 3; ++i) {
+      const int u = st + 192 * i;
+      if (u < 512)
+        kraw[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                rk, ((u >> 4) * D + (u & 15) * 8) * 2, c0 * D * 2, 0));
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      kw[i] = __builtin_amdgcn_raw_buffer_load_b32(rk, ((8 * ko + i) * D + 2 * kp2) * 2, c0 * D * 2, 0);
+    for (int i = 0; i < 2; ++i) {
+      const int p = st + 192 * i;
+      if (p < 256) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      vw[i] = __builtin_amdgcn_raw_buffer_load_b32(rv, ((4 * vo + i) * D + DH * half + 2 * vp2) * 2,
-                                                   c0 * D * 2, 0);
-    graw = ldf(rg, (tid & (C - 1)) * 4, c0 * 4);
-    braw = ldf(rb, (tid & (C - 1)) * 4, c0 * 4);
-  };
-  fetch(0);
-
-  for (int t0 = 0; t0 < W; t0 += C) {
-    // ---- stage: keys (both layouts), this half's values, beta, the gates' running sum
+        for (int j = 0; j < 8; ++j)
+          kw[i][j] = __builtin_amdgcn_raw_buffer_load_b32(rk, ((8 * (p >> 6) + j) * D + 2 * (p & 63)) * 2,
+                                                          c0 * D * 2, 0);
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
-      *reinterpret_cast<uint4*>(sK + t * SK + c8) = kraw[u];
-    }
-    {
-      uint32_t lo[4], hi[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        lo[i] = __builtin_amdgcn_perm(kw[2 * i + 1], kw[2 * i], 0x05040100u);
-        hi[i] = __builtin_amdgcn_perm(kw[2 * i + 1], kw[2 * i], 0x07060302u);
+        for (int j = 0; j < 4; ++j)
+          vw[i][j] = __builtin_amdgcn_raw_buffer_load_b32(
+              rv, ((4 * (p >> 5) + j) * D + DH * half + 2 * (p & 31)) * 2, c0 * D * 2, 0);
       }
-      *reinterpret_cast<uint4*>(sKT + (2 * kp2) * SV + 8 * ko) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-      *reinterpret_cast<uint4*>(sKT + (2 * kp2 + 1) * SV + 8 * ko) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
     }
-    {
-      const uint32_t lo0 = __builtin_amdgcn_perm(vw[1], vw[0], 0x05040100u);
-      const uint32_t lo1 = __builtin_amdgcn_perm(vw[3], vw[2], 0x05040100u);
-      const uint32_t hi0 = __builtin_amdgcn_perm(vw[1], vw[0], 0x07060302u);
-      const uint32_t hi1 = __builtin_amdgcn_perm(vw[3], vw[2], 0x07060302u);
-      *reinterpret_cast<uint2*>(sVT + (2 * vp2) * SV + 4 * vo) = make_uint2(lo0, lo1);
-      *reinterpret_cast<uint2*>(sVT + (2 * vp2 + 1) * SV + 4 * vo) = make_uint2(hi0, hi1);
+    graw = ldf(rg, (st & (C - 1)) * 4, c0 * 4);
+    braw = ldf(rb, (st & (C - 1)) * 4, c0 * 4);
+  };
+  auto stage = [&](int b) {
+    uint16_t* sK = bK(b);
+    uint16_t* sKT = bKT(b);
+    uint16_t* sVT = bVT(b);
+#pragma unroll
+    for (int i = 0; i < 3; ++i) {
+      const int u = st + 192 * i;
+      if (u < 512) *reinterpret_cast<uint4*>(sK + (u >> 4) * SK + (u & 15) * 8) = kraw[i];
     }
-    if (w == 0) {   // inclusive running sum over the 32 tokens by lane shuffles
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int p = st + 192 * i;
+      if (p < 256) {
+        uint32_t lo[4], hi[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          lo[j] = __builtin_amdgcn_perm(kw[i][2 * j + 1], kw[i][2 * j], 0x05040100u);
+          hi[j] = __builtin_amdgcn_perm(kw[i][2 * j + 1], kw[i][2 * j], 0x07060302u);
+        }
+        const int c2 = 2 * (p & 63), t8 = 8 * (p >> 6);
+        *reinterpret_cast<uint4*>(sKT + c2 * SV + t8) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+        *reinterpret_cast<uint4*>(sKT + (c2 + 1) * SV + t8) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+        const uint32_t vlo0 = __builtin_amdgcn_perm(vw[i][1], vw[i][0], 0x05040100u);
+        const uint32_t vlo1 = __builtin_amdgcn_perm(vw[i][3], vw[i][2], 0x05040100u);
+        const uint32_t vhi0 = __builtin_amdgcn_perm(vw[i][1], vw[i][0], 0x07060302u);
+        const uint32_t vhi1 = __builtin_amdgcn_perm(vw[i][3], vw[i][2], 0x07060302u);
+        const int v2 = 2 * (p & 31), t4 = 4 * (p >> 5);
+        *reinterpret_cast<uint2*>(sVT + v2 * SV + t4) = make_uint2(vlo0, vlo1);
+        *reinterpret_cast<uint2*>(sVT + (v2 + 1) * SV + t4) = make_uint2(vhi0, vhi1);
+      }
+    }
+    if (w == 1) {   // inclusive running sum of the log2 gates by lane shuffles
       float x = lane < C ? fmaxf(graw, kGateFloor) * kLog2e : 0.f;
 #pragma unroll
       for (int d = 1; d < C; d <<= 1) {
@@ -220,24 +240,31 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       }
       const float gc = __shfl(x, C - 1);
       if (lane < C) {
-        sG[lane] = x;
-        sEG[lane] = ex2(x);
-        sEH[lane] = ex2(gc - x);
-        sBeta[lane] = braw;
+        bG(b)[lane] = x;
+        bEG(b)[lane] = ex2(x);
+        bEH(b)[lane] = ex2(gc - x);
+        bBeta(b)[lane] = braw;
       }
     }
-    __syncthreads();
-
-    // ---- A = Diag(beta) (K K^T with decays), strictly lower: waves 0-2, one tile each;
-    // X = Diag(2^G) (K S') on every wave's own columns
-    if (w < 3) {
-      const int ti = w == 0 ? 0 : 1, si = w == 2 ? 1 : 0;
+  };
+  // A of the chunk in buffer b, strictly lower, tiles (0,0), (1,0), (1,1): wave 2 takes
+  // the first two, wave 3 the third
+  auto a_tiles = [&](int b) {
+    const uint16_t* sK = bK(b);
+    const float* sG = bG(b);
+    const float* sBeta = bBeta(b);
+    float* sA = bA(b);
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      const int tile = w == 2 ? tt : 2;
+      if (w == 3 && tt == 1) break;
+      const int ti = tile == 0 ? 0 : 1, si = tile == 2 ? 1 : 0;
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(sK + (16 * ti + r) * SK + 32 * kk + 8 * q);
-        const bf16x8 b = *reinterpret_cast<const bf16x8*>(sK + (16 * si + r) * SK + 32 * kk + 8 * q);
-        acc = mma(a, b, acc);
+        const bf16x8 a8 = *reinterpret_cast<const bf16x8*>(sK + (16 * ti + r) * SK + 32 * kk + 8 * q);
+        const bf16x8 b8 = *reinterpret_cast<const bf16x8*>(sK + (16 * si + r) * SK + 32 * kk + 8 * q);
+        acc = mma(a8, b8, acc);
       }
       const int s = 16 * si + r;
 #pragma unroll
@@ -246,7 +273,12 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
         sA[t * C + s] = s < t ? sBeta[t] * acc[i] * ex2(sG[t] - sG[s]) : 0.f;
       }
     }
-    f32x4 X[2] = {};
+  };
+  // X = Diag(2^G) (K S') on this wave's columns
+  auto form_x = [&](int b, f32x4* X) {
+    const __bf16* sK = reinterpret_cast<const __bf16*>(bK(b));
+    X[0] = f32x4{0.f, 0.f, 0.f, 0.f};
+    X[1] = X[0];
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       bf16x8 sh, slo;
@@ -258,73 +290,97 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       }
 #pragma unroll
       for (int mu = 0; mu < 2; ++mu) {
-        const bf16x8 kk8 = ld_op(reinterpret_cast<const __bf16*>(sK) + (16 * mu + r) * SK + 32 * kk + 4 * q);
+        const bf16x8 kk8 = ld_op(sK + (16 * mu + r) * SK + 32 * kk + 4 * q);
         X[mu] = mma(kk8, slo, X[mu]);
         X[mu] = mma(kk8, sh, X[mu]);
       }
     }
 #pragma unroll
-    for (int mu = 0; mu < 2; ++mu) {
-      const f32x4 eg = *reinterpret_cast<const f32x4*>(sEG + 16 * mu + 4 * q);
-      X[mu] *= eg;
-    }
-    __syncthreads();
+    for (int mu = 0; mu < 2; ++mu) X[mu] *= *reinterpret_cast<const f32x4*>(bEG(b) + 16 * mu + 4 * q);
+  };
 
-    // ---- T = (I + A)^{-1}: diagonal 16x16 blocks by forward substitution -----------
-    if (w == 0 && lane < 32) {
-      const int base = 16 * (lane >> 4), s = lane & 15;
-      float x[16];
-#pragma unroll
-      for (int t = 0; t < 16; ++t) {
-        float a = (t == s) ? 1.f : 0.f;
-#pragma unroll
-        for (int rr = 0; rr < t; ++rr) a = fmaf(-sA[(base + t) * C + base + rr], x[rr], a);
-        x[t] = a;
-        sT[(base + t) * C + base + s] = a;
-      }
-    }
-    // the next chunk's inputs load while this chunk finishes (zeros past the window)
-    fetch(t0 + C);
-    __syncthreads();
+  // prologue: chunk 0 staged and its A built; chunk 1 in flight
+  if (w > 0) fetch(0);
+  if (w > 0) stage(0);
+  __syncthreads();
+  if (w >= 2) a_tiles(0);
+  if (w > 0) fetch(C);
+  __syncthreads();
 
-    // ---- T' = T Diag(beta), split hi/lo; wave 1 forms T10 = -T11 (A10 T00) ---------
-    if (w == 1) {
-      f32x4 y = {0.f, 0.f, 0.f, 0.f};
+  for (int t0 = 0, b = 0; t0 < W; t0 += C, b ^= 1) {
+    const bool more = t0 + C < W;
+    f32x4 X[2];
+    // ---- P1: T = (I + A)^{-1} diagonal blocks (wave 0) | X and the next chunk's staging
+    if (w == 0) {
+      if (lane < 32) {
+        const float* sA = bA(b);
+        const int base = 16 * (lane >> 4), s = lane & 15;
+        float x[16];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        y = mma32(sA[(16 + r) * C + 4 * q + i], sT[(4 * q + i) * C + r], y);
-      f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < 16; ++t) {
+          float a = (t == s) ? 1.f : 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) z = mma32(sT[(16 + r) * C + 16 + 4 * q + i], y[i], z);
-      const float br = sBeta[r];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int t = 16 + 4 * q + i;
-        __bf16 a, b;
-        split(-z[i] * br, a, b);
-        sTPH[t * SP + r] = a;
-        sTPL[t * SP + r] = b;
+          for (int rr = 0; rr < t; ++rr) a = fmaf(-sA[(base + t) * C + base + rr], x[rr], a);
+          x[t] = a;
+          sT[(base + t) * C + base + s] = a;
+        }
       }
     } else {
-      const int lt = w == 0 ? tid : tid - 64;       // 0 .. 191
+      form_x(b, X);
+      if (more) stage(b ^ 1);
+    }
+    __syncthreads();
+
+    // ---- P2: X (wave 0) | T' = T Diag(beta) split, T10 = -T11 (A10 T00) on wave 1 |
+    //          the next chunk's A tiles (waves 2-3) | loads of the chunk after next
+    {
+      const float* sA = bA(b);
+      const float* sBeta = bBeta(b);
+      if (w == 0) {
+        form_x(b, X);
+      } else if (w == 1) {
+        f32x4 y = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        // 768 entries outside block (1,0): rows 0..15 whole, rows 16..31 columns 16..31
-        const int e = lt + 192 * u;
-        const int t = e < 512 ? e >> 5 : 16 + ((e - 512) >> 4);
-        const int s = e < 512 ? e & 31 : 16 + ((e - 512) & 15);
-        const float val = s <= t ? sT[t * C + s] * sBeta[s] : 0.f;
-        __bf16 a, b;
-        split(val, a, b);
-        sTPH[t * SP + s] = a;
-        sTPL[t * SP + s] = b;
+        for (int i = 0; i < 4; ++i)
+          y = mma32(sA[(16 + r) * C + 4 * q + i], sT[(4 * q + i) * C + r], y);
+        f32x4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) z = mma32(sT[(16 + r) * C + 16 + 4 * q + i], y[i], z);
+        const float br = sBeta[r];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t = 16 + 4 * q + i;
+          __bf16 a, bb;
+          split(-z[i] * br, a, bb);
+          sTPH[t * SP + r] = a;
+          sTPL[t * SP + r] = bb;
+        }
+      }
+      if (w >= 1) {
+        // 768 entries outside block (1,0): rows 0..15 whole, rows 16..31 columns 16..31,
+        // over waves 1-3 (wave 1 after its T10)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int e = st + 192 * u;
+          const int t = e < 512 ? e >> 5 : 16 + ((e - 512) >> 4);
+          const int s = e < 512 ? e & 31 : 16 + ((e - 512) & 15);
+          const float val = s <= t ? sT[t * C + s] * sBeta[s] : 0.f;
+          __bf16 a, bb;
+          split(val, a, bb);
+          sTPH[t * SP + s] = a;
+          sTPL[t * SP + s] = bb;
+        }
+        if (w >= 2 && more) a_tiles(b ^ 1);
+        if (t0 + 2 * C < W) fetch(t0 + 2 * C);
       }
     }
     __syncthreads();
 
-    // ---- U = T' (V - X), then Diag(2^{G_C - G}) U -----------------------------------
-    f32x4 U[2];
+    // ---- P3: U = T' (V - X), Diag(2^{G_C - G}) U, S' <- 2^{G_C} S' + K^T U --------------
     {
+      const uint16_t* sVT = bVT(b);
+      const float* sEH = bEH(b);
+      f32x4 U[2];
       bf16x8 yh, yl;
       float x[8];
 #pragma unroll
@@ -345,22 +401,21 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
         U[mu] = mma(ah, yh, c);
         U[mu] *= *reinterpret_cast<const f32x4*>(sEH + 16 * mu + 4 * q);
       }
-    }
-
-    // ---- S' <- 2^{G_C} S' + K^T U -----------------------------------------------------
-    bf16x8 uh, ul;
-    {
-      float x[8];
+      bf16x8 uh, ul;
+      {
+        float xu[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = U[e >> 2][e & 3];
-      split8(x, uh, ul);
-    }
-    const float gam = sEG[C - 1];
+        for (int e = 0; e < 8; ++e) xu[e] = U[e >> 2][e & 3];
+        split8(xu, uh, ul);
+      }
+      const float gam = bEG(b)[C - 1];
+      const __bf16* sKT = reinterpret_cast<const __bf16*>(bKT(b));
 #pragma unroll
-    for (int mt = 0; mt < 8; ++mt) {
-      const bf16x8 kt8 = ld_op(reinterpret_cast<const __bf16*>(sKT) + (16 * mt + r) * SV + 4 * q);
-      S[mt] = mma(kt8, ul, S[mt] * gam);
-      S[mt] = mma(kt8, uh, S[mt]);
+      for (int mt = 0; mt < 8; ++mt) {
+        const bf16x8 kt8 = ld_op(sKT + (16 * mt + r) * SV + 4 * q);
+        S[mt] = mma(kt8, ul, S[mt] * gam);
+        S[mt] = mma(kt8, uh, S[mt]);
+      }
     }
     __syncthreads();
   }
