@@ -457,11 +457,16 @@ def bench_gdn(torch, args):
     ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
     t = {k_: timer.mean_ms(k_) for k_ in ("pack", "restore", "refresh_all_layers")}
     bp, br = 2 * R * dv * 4 * n, (R + rows) * dv * 4 * n
-    om_heads = int((plan["inv_row"].reshape(-1, sh.dk) < 0).all(axis=1).sum())
+    omitted = (plan["inv_row"].reshape(sh.n_layers, sh.n_heads, sh.dk) < 0).all(axis=2)
+    om_heads = int(omitted.sum())
     heads = wl.n_req * om_heads
-    # per refreshed head: k, v (bf16), g, beta (fp32), the restored head read and written
-    per_head = 2 * W * sh.dk + 2 * W * dv + 4 * W + 4 * W + 2 * 4 * sh.dk * dv
-    bytes_ref = heads * per_head
+    # key heads some omitted v-head of their layer reads (v-heads of a group share one)
+    key_heads = wl.n_req * sum(len(set(np.flatnonzero(o) // (sh.n_heads // sh.n_qk_heads)))
+                               for o in omitted)
+    # per refreshed head: v (bf16), g, beta (fp32), the restored head read and written; per
+    # key head read: k (bf16)
+    per_head = 2 * W * dv + 4 * W + 4 * W + 2 * 4 * sh.dk * dv
+    bytes_ref = heads * per_head + key_heads * 2 * W * sh.dk
     ach = bytes_ref / (t["refresh_all_layers"] / 1e3) / 1e9          # GB/s
     flops = 5.0 * sh.dk * dv * W * heads
     return {
@@ -474,9 +479,11 @@ def bench_gdn(torch, args):
                                f"checkpoints (12 of 32 heads kept), refresh {wl.n_req} requests x "
                                f"{om_heads} omitted heads W={W}"},
         "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": ach / HBM_PEAK_GBPS, "traffic": None, "kernel": "refresh",
+                     "frac": ach / HBM_PEAK_GBPS, "traffic": measured_traffic("qwen_gdn/refresh"),
+                     "kernel": "refresh",
                      "work_per_launch": f"{bytes_ref // wl.n_layers} B per layer launch "
-                                        f"({heads // wl.n_layers} heads)",
+                                        f"({heads // wl.n_layers} heads, "
+                                        f"{key_heads / wl.n_layers:.1f} key heads)",
                      "recurrence_TFLOPs": flops / (t["refresh_all_layers"] / 1e3) / 1e12},
         "kernels": {"pack": {"ms": t["pack"], "GBps": bp / t["pack"] / 1e6},
                     "restore": {"ms": t["restore"], "GBps": br / t["restore"] / 1e6},

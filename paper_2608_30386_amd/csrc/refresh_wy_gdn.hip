@@ -115,6 +115,15 @@ __device__ inline bf16x8 ld_op(const __bf16* p) {
   return cat(*reinterpret_cast<const bf16x4*>(p), *reinterpret_cast<const bf16x4*>(p + 16));
 }
 
+// Blocks are dealt to the eight XCDs in turn (block b starts on XCD b mod 8).  Renumber
+// them so that each XCD takes a contiguous range of (request, head, half) items: the
+// blocks that read one key head (both halves of every v-head in its group) then sit on
+// the same XCD and share its L2.  A bijection whenever the grid is a multiple of 8.
+__device__ inline int xcd_major(int b, int n_blocks) {
+  if (n_blocks & 7) return b;
+  return (b & 7) * (n_blocks >> 3) + (b >> 3);
+}
+
 __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     int H, int Hqk, int layer, int L, const int32_t* __restrict__ inv_row,
     float* __restrict__ states, int64_t n_pool, const int32_t* __restrict__ slot,
@@ -133,8 +142,9 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
   auto bEH = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_EH); };
   auto bBeta = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_BETA); };
 
-  const int half = blockIdx.x & 1;
-  const int nh = blockIdx.x >> 1;
+  const int item = xcd_major(blockIdx.x, gridDim.x);
+  const int half = item & 1;
+  const int nh = item >> 1;
   const int n = nh / H;
   const int h = nh - n * H;
   const int tid = threadIdx.x;
