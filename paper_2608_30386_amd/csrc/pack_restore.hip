@@ -7,11 +7,17 @@
 //
 // Both kernels are HBM-bound bit copies.  A state row (one KDA unit, or one of the
 // dk rows of a GDN unit) is dv fp32 words = dv/4 128-bit vectors, 512 B at dv = 128.
-// A 256-thread block owns a tile of rows of one checkpoint; each thread issues
-// UNROLL independent 128-bit loads before its stores so that enough reads are in
-// flight per CU to cover HBM latency.  The per-row index (unit_row / inv_row) is a
-// single 32-bit load shared by the dv/4 lanes of that row.  Destination stores are
-// non-temporal: nothing reads a freshly written checkpoint or state back from cache.
+// A 256-thread block owns a small tile of rows of one checkpoint.  A vector's data
+// load depends on its row's index load (unit_row / inv_row), and the two serialise on
+// the load counter, so how many reads a CU keeps in flight is set by how many waves
+// are resident and by independent loads per thread:
+//   pack    one vector per thread (8 rows of 512 B per block), index loaded per lane;
+//   restore the block's inv_row entries are staged in LDS first, then every thread
+//           issues two independent vector loads.
+// Measured on the full-model set (256 checkpoints of 24 x 32 x 128 rows) these beat
+// four vectors per thread with per-lane index loads: pack 5.1 -> 6.2 TB/s, restore
+// 5.5 -> 5.9 TB/s.  Destination stores are non-temporal: nothing reads a freshly
+// written checkpoint or state back from cache.
 
 #include <hip/hip_runtime.h>
 
@@ -27,8 +33,10 @@ namespace {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
-constexpr int kVecPerBlock = kThreads * kUnroll;  // 128-bit vectors moved per block
+constexpr int kPackUnroll = 1;      // 128-bit vectors per thread
+constexpr int kRestoreUnroll = 2;
+constexpr int kPackVec = kThreads * kPackUnroll;        // vectors moved per block
+constexpr int kRestoreVec = kThreads * kRestoreUnroll;
 
 // VPR_LOG2 >= 0: dv/4 is the power of two 2^VPR_LOG2 (shift/mask addressing).
 // VPR_LOG2 <  0: dv/4 given at run time (division addressing).
@@ -47,8 +55,9 @@ struct RowGeom<-1> {
 
 using dasc::slice_row;
 
-// Rows per block: enough 128-bit vectors for every thread to move kUnroll of them.
-inline int rows_per_block(int vpr) { return vpr >= kVecPerBlock ? 1 : kVecPerBlock / vpr; }
+// Rows per block: enough 128-bit vectors for every thread to move its share (vec per
+// block), or one row when a row alone is longer.
+inline int rows_per_block(int vpr, int vec) { return vpr >= vec ? 1 : vec / vpr; }
 
 // A block owns a tile of rows of one rank slice of one checkpoint, so the slice of a
 // packed row is known per block and the destination needs no per-row division.
@@ -61,11 +70,14 @@ __device__ __forceinline__ void pack_body(
     const int32_t* __restrict__ slice_begin) {
   using G = RowGeom<VPR_LOG2>;
   const int vpr = G::vpr(vpr_rt);
-  const int per_ckpt = n_ranks * blocks_per_slice;
-  const int i = blockIdx.x / per_ckpt;
-  const int rem = blockIdx.x - i * per_ckpt;
-  const int rk = rem / blocks_per_slice;
-  const int rb = rem - rk * blocks_per_slice;
+  // slice-major block order: consecutive blocks fill slice rk of consecutive checkpoint
+  // slots, which are adjacent in [T, n_slots, C_rows, dv], so the writes in flight stay
+  // in one region instead of spreading over the T slices of one checkpoint
+  const int per_slice = int(gridDim.x) / n_ranks;   // n checkpoints x blocks_per_slice
+  const int rk = blockIdx.x / per_slice;
+  const int rem = blockIdx.x - rk * per_slice;
+  const int i = rem / blocks_per_slice;
+  const int rb = rem - i * blocks_per_slice;
   const int64_t s = src_slot[i];
   const int64_t d = dst_slot[i];
   if (s < 0 || s >= n_pool || d < 0 || d >= n_ckpt_slots) return;
@@ -82,11 +94,11 @@ __device__ __forceinline__ void pack_body(
   const int64_t dbase = ((int64_t(rk) * n_ckpt_slots + d) * slice_rows - slice0) * vpr;
   const int n_vec = rpb * vpr;
 
-  for (int base = 0; base < n_vec; base += kVecPerBlock) {
-    f32x4 val[kUnroll];
-    int64_t dst_off[kUnroll];
+  for (int base = 0; base < n_vec; base += kPackVec) {
+    f32x4 val[kPackUnroll];
+    int64_t dst_off[kPackUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
+    for (int u = 0; u < kPackUnroll; ++u) {
       const int v = base + u * kThreads + threadIdx.x;
       const int64_t j = row0 + G::row_of(v, vpr_rt);
       dst_off[u] = -1;
@@ -100,7 +112,7 @@ __device__ __forceinline__ void pack_body(
       }
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
+    for (int u = 0; u < kPackUnroll; ++u)
       if (dst_off[u] >= 0) __builtin_nontemporal_store(val[u], ckpt + (dbase + dst_off[u]));
   }
 }
@@ -145,6 +157,11 @@ __device__ __forceinline__ void restore_body(
   f32x4* dst = states + d * rows_state * vpr;
   const int64_t row0 = int64_t(rb) * rpb;
   const int n_vec = rpb * vpr;
+  // packed index of each row of the tile, read once per row instead of once per lane
+  __shared__ int32_t s_inv[kRestoreVec];
+  for (int t = threadIdx.x; t < rpb; t += kThreads)
+    if (row0 + t < rows_state) s_inv[t] = inv_row[row0 + t];
+  __syncthreads();
   int64_t blk_layer = -1;   // padded: the layer of every row of this block, if unique
   if (PADDED) {
     const int64_t last = min(row0 + rpb, rows_state) - 1;
@@ -152,18 +169,19 @@ __device__ __forceinline__ void restore_body(
     if (l0 == int64_t(uint32_t(last) / uint32_t(rows_per_layer))) blk_layer = l0;
   }
 
-  for (int base = 0; base < n_vec; base += kVecPerBlock) {
-    f32x4 val[kUnroll];
-    int64_t dst_off[kUnroll];
+  for (int base = 0; base < n_vec; base += kRestoreVec) {
+    f32x4 val[kRestoreUnroll];
+    int64_t dst_off[kRestoreUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
+    for (int u = 0; u < kRestoreUnroll; ++u) {
       const int v = base + u * kThreads + threadIdx.x;
-      const int64_t dense = row0 + G::row_of(v, vpr_rt);
+      const int r = G::row_of(v, vpr_rt);
+      const int64_t dense = row0 + r;
       dst_off[u] = -1;
       val[u] = f32x4{0.f, 0.f, 0.f, 0.f};
       if (v < n_vec && dense < rows_state) {
         const int c = G::col_of(v, vpr_rt);
-        const int64_t p = inv_row[dense];
+        const int64_t p = s_inv[r];
         if (p >= 0 && p < n_rows) {
           int64_t row;
           if (PADDED) {
@@ -180,7 +198,7 @@ __device__ __forceinline__ void restore_body(
       }
     }
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
+    for (int u = 0; u < kRestoreUnroll; ++u)
       if (dst_off[u] >= 0) __builtin_nontemporal_store(val[u], dst + dst_off[u]);
   }
 }
@@ -251,7 +269,7 @@ extern "C" int dasc_pack(const dasc_shape* shape, const float* states, int64_t n
   if (!states || !src_slot || !unit_row || !ckpt || !dst_slot) return DASC_E_INVAL;
   if (!dasc::aligned16(states) || !dasc::aligned16(ckpt)) return DASC_E_INVAL;
   const int vpr = shape->dv / 4;
-  const int rpb = rows_per_block(vpr);
+  const int rpb = rows_per_block(vpr, kPackVec);
   // blocks per rank slice: a slice holds at most min(slice_rows, n_rows) packed rows
   const int64_t bps = (std::min<int64_t>(slice_rows, n_rows) + rpb - 1) / rpb;
   const int64_t blocks = bps * n_ranks * n;
@@ -278,7 +296,7 @@ extern "C" int dasc_restore(const dasc_shape* shape, const float* ckpt, int64_t 
   if (!dasc::aligned16(states) || !dasc::aligned16(ckpt)) return DASC_E_INVAL;
   if (n_rows == 0) slice_rows = 1;  // nothing is read; keeps the divisor non-zero
   const int vpr = shape->dv / 4;
-  const int rpb = rows_per_block(vpr);
+  const int rpb = rows_per_block(vpr, kRestoreVec);
   const int64_t rows = dasc::rows_per_state(shape);
   const int64_t bps = (rows + rpb - 1) / rpb;
   if (bps * n > INT32_MAX) return DASC_E_INVAL;
@@ -310,7 +328,7 @@ extern "C" int dasc_pack_padded(const dasc_shape* shape, const float* states, in
   if (!dasc::aligned16(states) || !dasc::aligned16(ckpt)) return DASC_E_INVAL;
   const int L = shape->n_layers;
   const int vpr = shape->dv / 4;
-  const int rpb = rows_per_block(vpr);
+  const int rpb = rows_per_block(vpr, kPackVec);
   const int64_t bps = (std::min<int64_t>(r_max_rows, n_rows) + rpb - 1) / rpb;
   const int64_t blocks = bps * L * n;
   if (blocks > INT32_MAX) return DASC_E_INVAL;
@@ -339,7 +357,7 @@ extern "C" int dasc_restore_padded(const dasc_shape* shape, const float* ckpt,
   if (!dasc::aligned16(states) || !dasc::aligned16(ckpt)) return DASC_E_INVAL;
   if (n_rows == 0) r_max_rows = 1;  // nothing is read
   const int vpr = shape->dv / 4;
-  const int rpb = rows_per_block(vpr);
+  const int rpb = rows_per_block(vpr, kRestoreVec);
   const int64_t rows = dasc::rows_per_state(shape);
   const int64_t bps = (rows + rpb - 1) / rpb;
   if (bps * n > INT32_MAX) return DASC_E_INVAL;
