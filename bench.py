@@ -131,6 +131,19 @@ def main():
 
 # ---------------------------------------------------------------------------------------
 
+def timed_steps(torch, fn, args) -> float:
+    """Warm up, then wall-clock exactly args.steps calls between two synchronisations (ms
+    per call)."""
+    for _ in range(args.warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / args.steps
+
+
 def _setup_plan(wl):
     import paper_2608_30386_amd as D
     from workloads import log_lambda
@@ -175,21 +188,29 @@ def bench_headline(torch, args):
 
     timer = KernelTimer(torch)
 
+    def plain_step():
+        D.dasc_pack(sh, states, ids, unit_row, ckpt, ids)
+        D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R)
+        D.dasc_refresh(sh, 0, inv_row, active, req, k, v, g, beta, W)
+
     def step():
         timer.run("pack", lambda: D.dasc_pack(sh, states, ids, unit_row, ckpt, ids))
         timer.run("restore", lambda: D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R))
         timer.run("refresh", lambda: D.dasc_refresh(sh, 0, inv_row, active, req, k, v, g, beta, W))
 
+    # the timed steps are plain launches; events around each launch add about 10 us of
+    # GPU-side gap per kernel, so the per-kernel durations come from a second pass.
+    # (A HIP graph of the three launches replays slower here: 0.405 vs 0.357 ms.)
+    ms_step = timed_steps(torch, plain_step, args)
+
+    # per-kernel durations: HIP events around each launch, on the library's stream
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     timer.spans.clear()
-    t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = wall * 1e3 / args.steps
 
     # Load with refresh of the refreshed requests: dasc_restore + dasc_refresh (two launches)
     # against the fused dasc_restore_refresh (one launch, the same result bit for bit)
@@ -321,21 +342,24 @@ def bench_pack_restore_only(torch, args, name):
     ids = _i32(torch, np.arange(n))
     timer = KernelTimer(torch)
 
+    def plain_step():
+        D.dasc_pack(sh, states, ids, unit_row, ckpt, ids, n_ranks=T, slice_rows=C)
+        D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R, n_ranks=T, slice_rows=C)
+
     def step():
         timer.run("pack", lambda: D.dasc_pack(sh, states, ids, unit_row, ckpt, ids, n_ranks=T,
                                               slice_rows=C))
         timer.run("restore", lambda: D.dasc_restore(sh, ckpt, ids, inv_row, active, ids,
                                                     n_rows=R, n_ranks=T, slice_rows=C))
 
+    ms_step = timed_steps(torch, plain_step, args)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     timer.spans.clear()
-    t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
-    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
     bp = 2 * R * dv * 4 * n
     br = (R + rows) * dv * 4 * n
     t = {k_: timer.mean_ms(k_) for k_ in ("pack", "restore")}
@@ -437,24 +461,28 @@ def bench_gdn(torch, args):
                        torch.from_numpy(inp["g"]).cuda(), torch.from_numpy(inp["beta"]).cuda()))
     timer = KernelTimer(torch)
 
+    def ref():
+        for l, (k, v, g, b) in enumerate(layers):
+            D.dasc_refresh(sh, l, inv_row, active, req, k, v, g, b, W)
+
+    def plain_step():
+        D.dasc_pack(sh, states, ids, unit_row, ckpt, ids)
+        D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R)
+        ref()
+
     def step():
         timer.run("pack", lambda: D.dasc_pack(sh, states, ids, unit_row, ckpt, ids))
         timer.run("restore", lambda: D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R))
-
-        def ref():
-            for l, (k, v, g, b) in enumerate(layers):
-                D.dasc_refresh(sh, l, inv_row, active, req, k, v, g, b, W)
         timer.run("refresh_all_layers", ref)
 
+    ms_step = timed_steps(torch, plain_step, args)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     timer.spans.clear()
-    t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
-    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
     t = {k_: timer.mean_ms(k_) for k_ in ("pack", "restore", "refresh_all_layers")}
     bp, br = 2 * R * dv * 4 * n, (R + rows) * dv * 4 * n
     omitted = (plan["inv_row"].reshape(sh.n_layers, sh.n_heads, sh.dk) < 0).all(axis=2)
