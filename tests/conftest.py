@@ -14,7 +14,7 @@ def pytest_configure(config):
 
 
 def pytest_collection_modifyitems(config, items):
-    # GPU tests run on the GPU machine only; elsewhere they are skipped, not failed.
+    # GPU tests need a GPU; on a machine without one they are skipped, not failed.
     try:
         import torch
         has_gpu = torch.cuda.is_available()
