@@ -11,7 +11,8 @@
 //
 // Work split: one 256-thread block per (request, head); wave w owns value columns
 // [32w, 32w + 32) of S' (128 x 32 fp32 = 16 MFMA accumulator tiles held in VGPRs for
-// the whole replay).  Everything that does not depend on S' (cumulative decays, K_G,
+// the whole replay), tile nt holding the columns 32w + 2r + nt (r = lane % 16), so that
+// a lane's values for both tiles are one 32-bit word per token.  Everything that does not depend on S' (cumulative decays, K_G,
 // K_H, A, T') is built cooperatively in LDS each chunk; then each wave runs its three
 // chained contractions K_G S', T'(V - .), K_H^T U on its own columns.
 //
@@ -82,8 +83,7 @@ constexpr int OFF_K = OFF_G + C * SG * 4;      // bf16 [C][SK]  -> later T, T'
 constexpr int OFF_T = OFF_K;                   // f32  [C][C]
 constexpr int OFF_TPH = OFF_K + C * C * 4;     // bf16 [C][SP]
 constexpr int OFF_TPL = OFF_TPH + C * SP * 2;
-constexpr int OFF_VT = OFF_K + C * SK * 2;     // bf16 [D][SV]
-constexpr int OFF_KGH = OFF_VT + D * SV * 2;   // bf16 [C][SK]
+constexpr int OFF_KGH = OFF_K + C * SK * 2;    // bf16 [C][SK]
 constexpr int OFF_KGL = OFF_KGH + C * SK * 2;
 constexpr int OFF_KHH = OFF_KGL + C * SK * 2;  // bf16 [D][SV]
 constexpr int OFF_KHL = OFF_KHH + D * SV * 2;
@@ -163,7 +163,6 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   float* sG = reinterpret_cast<float*>(smem + OFF_G);
   uint16_t* sK = reinterpret_cast<uint16_t*>(smem + OFF_K);
   float* sT = reinterpret_cast<float*>(smem + OFF_T);
-  uint16_t* sVT = reinterpret_cast<uint16_t*>(smem + OFF_VT);
   __bf16* sKGH = reinterpret_cast<__bf16*>(smem + OFF_KGH);
   __bf16* sKGL = reinterpret_cast<__bf16*>(smem + OFF_KGL);
   __bf16* sKHH = reinterpret_cast<__bf16*>(smem + OFF_KHH);
@@ -228,7 +227,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int c = 16 * mt + 4 * q + i, j = 32 * w + 16 * nt + r;
+        const int c = 16 * mt + 4 * q + i, j = 32 * w + 2 * r + nt;
         if (FUSED) {
           // the restored value; a kept row is final already and is stored right away,
           // while the replay runs
@@ -255,19 +254,12 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   const int ch = tid >> 1;
   const int hf = tid & 1;
 
-  // Gates, keys, values and beta of one chunk as this thread loads them; the next
-  // chunk's are issued one chunk ahead.  Values come as column pairs: thread
-  // (octet o = tid / 64, pair p = tid % 64) holds columns 2p, 2p + 1 of tokens 8o .. 8o+7,
-  // so each load instruction reads one whole 256-byte token row.
-  const int vo = tid >> 6, vpair = tid & 63;
+  // Gates, keys and beta of one chunk as this thread loads them; the next chunk's are
+  // issued one chunk ahead.
   float graw[16];
   uint4 kraw[2];
-  uint32_t vw[8];
   float braw;
   auto fetch = [&](int c0) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      vw[i] = __builtin_amdgcn_raw_buffer_load_b32(rv, ((8 * vo + i) * D + 2 * vpair) * 2, c0 * D * 2, 0);
 #pragma unroll
     for (int i = 0; i < 16; ++i)
       graw[i] = PER_CHANNEL ? ldf(rg, ((16 * hf + i) * D + ch) * 4, c0 * D * 4)
@@ -279,10 +271,24 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     }
     braw = ldf(rb, (tid & (C - 1)) * 4, c0 * 4);
   };
+  // Values stay in registers in the layout the U phase consumes: lane (q, r) of wave w
+  // holds, for tokens 16 mu + 4q + i, the word with columns 32w + 2r (low half) and
+  // 32w + 2r + 1 (high half) -- its two S' tiles.  The next chunk's are loaded as soon as
+  // U has read this chunk's.
+  uint32_t vreg[2][4];
+  auto fetch_v = [&](int c0) {
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        vreg[mu][i] = __builtin_amdgcn_raw_buffer_load_b32(
+            rv, ((16 * mu + 4 * q + i) * D + 32 * w + 2 * r) * 2, c0 * D * 2, 0);
+  };
   fetch(0);
+  fetch_v(0);
 
   for (int t0 = 0; t0 < W; t0 += C) {
-    // ---- values of this chunk (issued first), then the prefetched gates, keys, beta ---
+    // ---- stage the prefetched gates (running sums), keys and beta -----------------------
     float Gl[16];
     {
       float run = 0.f;
@@ -300,16 +306,6 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     for (int u = 0; u < 2; ++u) {
       const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
       *reinterpret_cast<uint4*>(sK + t * SK + c8) = kraw[u];
-    }
-    {  // columns 2p, 2p + 1, tokens 8o .. 8o+7 -> two transposed row segments
-      uint32_t lo[4], hi[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        lo[i] = __builtin_amdgcn_perm(vw[2 * i + 1], vw[2 * i], 0x05040100u);  // low halves
-        hi[i] = __builtin_amdgcn_perm(vw[2 * i + 1], vw[2 * i], 0x07060302u);  // high halves
-      }
-      *reinterpret_cast<uint4*>(sVT + (2 * vpair) * SV + 8 * vo) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-      *reinterpret_cast<uint4*>(sVT + (2 * vpair + 1) * SV + 8 * vo) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
     }
     if (tid < C) sBeta[tid] = braw;
 #pragma unroll
@@ -479,18 +475,17 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       bf16x8 yh[2], yl[2];
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        const int j = 32 * w + 16 * nt + r;
         float x[8];
 #pragma unroll
-        for (int mu = 0; mu < 2; ++mu) {
-          const uint2 vv = *reinterpret_cast<const uint2*>(sVT + j * SV + 16 * mu + 4 * q);
-          const float vf[4] = {__uint_as_float(vv.x << 16), __uint_as_float(vv.x & 0xFFFF0000u),
-                               __uint_as_float(vv.y << 16), __uint_as_float(vv.y & 0xFFFF0000u)};
+        for (int mu = 0; mu < 2; ++mu)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) x[4 * mu + i] = vf[i] - X[mu][nt][i];
-        }
+          for (int i = 0; i < 4; ++i) {
+            const uint32_t vv = vreg[mu][i];
+            x[4 * mu + i] = __uint_as_float(nt ? (vv & 0xFFFF0000u) : (vv << 16)) - X[mu][nt][i];
+          }
         split8(x, yh[nt], yl[nt]);
       }
+      fetch_v(t0 + C);   // the next chunk's values (zeros past the window)
 #pragma unroll
       for (int mu = 0; mu < 2; ++mu) {
         const int o = (16 * mu + r) * SP + 4 * q;
@@ -535,7 +530,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       // live through the replay and spill
       if (reinterpret_cast<const volatile int32_t*>(inv_row)[head_row + c] < 0) {
 #pragma unroll
-        for (int nt = 0; nt < 2; ++nt) S_head[int64_t(c) * D + 32 * w + 16 * nt + r] = S[mt][nt][i];
+        for (int nt = 0; nt < 2; ++nt) S_head[int64_t(c) * D + 32 * w + 2 * r + nt] = S[mt][nt][i];
       }
     }
 }
