@@ -321,7 +321,10 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       const int rf = w == 0 ? 8 : (w == 1 ? 15 : 24);   // reference token of the tile
       const int tr = 16 * ti + r, sr = 16 * si + r;
       f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
+      // fully unrolled the reads and exponentials overlap best; the fused variant keeps
+      // two steps, where the checkpoint row table already presses on registers
+      constexpr int kAUnroll = FUSED ? 2 : 8;
+#pragma unroll kAUnroll
       for (int j = 0; j < 8; ++j) {
         const int c0 = 16 * j + 4 * q;
         const f32x4 gt = *reinterpret_cast<const f32x4*>(sG + tr * SG + c0);
