@@ -64,16 +64,24 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(key: str):
-    """HBM bytes per launch from the committed counter summary, if it matches this source."""
+def _counter_summary():
+    """The committed counter summary, if it was taken on the current kernel sources."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
-        return None
+        return {}
     with open(path) as fh:
         t = json.load(fh)
-    if t.get("source_hash") != kernel_source_hash():
-        return None
-    return t.get("kernels", {}).get(key)
+    return t if t.get("source_hash") == kernel_source_hash() else {}
+
+
+def measured_traffic(key: str):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, scaled), or None."""
+    return _counter_summary().get("kernels", {}).get(key)
+
+
+def measured_util(key: str, what: str):
+    """MFMA-busy or VALU-active fraction of the kernel's SIMD cycles, or None."""
+    return _counter_summary().get("utilisation", {}).get(key, {}).get(what)
 
 
 class KernelTimer:
@@ -280,7 +288,9 @@ def bench_headline(torch, args):
                      "traffic": traffic, "kernel": "refresh",
                      "work_per_launch": f"{bytes_refresh} B = per refreshed head: k, v (bf16), g, "
                                         "beta (fp32), restored state read, omitted rows written",
-                     "mfma_frac": flops_refresh / (t["refresh"] / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS},
+                     "mfma_frac": flops_refresh / (t["refresh"] / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+                     "mfma_busy": measured_util("kimi_headline/refresh", "mfma_busy"),
+                     "valu_active": measured_util("kimi_headline/refresh", "valu_active")},
         "kernels": kernels,
         "pack_restore_GBps": (bytes_pack + bytes_restore) / (t["pack"] + t["restore"]) / 1e6,
         "plan_host_ms": plan_s * 1e3,
@@ -512,7 +522,9 @@ def bench_gdn(torch, args):
                      "work_per_launch": f"{bytes_ref // wl.n_layers} B per layer launch "
                                         f"({heads // wl.n_layers} heads, "
                                         f"{key_heads / wl.n_layers:.1f} key heads)",
-                     "recurrence_TFLOPs": flops / (t["refresh_all_layers"] / 1e3) / 1e12},
+                     "recurrence_TFLOPs": flops / (t["refresh_all_layers"] / 1e3) / 1e12,
+                     "mfma_busy": measured_util("qwen_gdn/refresh", "mfma_busy"),
+                     "valu_active": measured_util("qwen_gdn/refresh", "valu_active")},
         "kernels": {"pack": {"ms": t["pack"], "GBps": bp / t["pack"] / 1e6},
                     "restore": {"ms": t["restore"], "GBps": br / t["restore"] / 1e6},
                     "refresh_all_layers": {"ms": t["refresh_all_layers"], "GBps": ach,
