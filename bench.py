@@ -493,7 +493,28 @@ def bench_gdn(torch, args):
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
-    t = {k_: timer.mean_ms(k_) for k_ in ("pack", "restore", "refresh_all_layers")}
+
+    # Load with refresh of the 8 requests: dasc_restore of their states + the 36 layer
+    # refreshes, against one dasc_restore_refresh per layer (each restores its own layer;
+    # the same bits)
+    def load_wr():
+        timer.run("restore_req", lambda: D.dasc_restore(sh, ckpt, req, inv_row, active, req, n_rows=R))
+        timer.run("refresh_req", ref)
+
+        def fused():
+            for l, (k, v, g, b) in enumerate(layers):
+                D.dasc_restore_refresh(sh, l, ckpt, req, inv_row, active, req, k, v, g, b, W, n_rows=R)
+        timer.run("restore_refresh", fused)
+
+    load_wr()
+    torch.cuda.synchronize()
+    for name in ("restore_req", "refresh_req", "restore_refresh"):
+        timer.spans[name].clear()
+    for _ in range(args.steps):
+        load_wr()
+    torch.cuda.synchronize()
+    t = {k_: timer.mean_ms(k_) for k_ in ("pack", "restore", "refresh_all_layers", "restore_req",
+                                          "refresh_req", "restore_refresh")}
     bp, br = 2 * R * dv * 4 * n, (R + rows) * dv * 4 * n
     omitted = (plan["inv_row"].reshape(sh.n_layers, sh.n_heads, sh.dk) < 0).all(axis=2)
     om_heads = int(omitted.sum())
@@ -528,7 +549,10 @@ def bench_gdn(torch, args):
         "kernels": {"pack": {"ms": t["pack"], "GBps": bp / t["pack"] / 1e6},
                     "restore": {"ms": t["restore"], "GBps": br / t["restore"] / 1e6},
                     "refresh_all_layers": {"ms": t["refresh_all_layers"], "GBps": ach,
-                                           "launches": wl.n_layers, "bytes": bytes_ref}},
+                                           "launches": wl.n_layers, "bytes": bytes_ref},
+                    "restore_refresh_fused": {"ms": t["restore_refresh"], "launches": wl.n_layers,
+                                              "unfused_ms": t["restore_req"] + t["refresh_req"],
+                                              "requests": wl.n_req}},
         "plan_host_ms": plan_s * 1e3,
     }
 

@@ -214,13 +214,24 @@ extern "C" int dasc_restore_refresh(const dasc_shape* shape, int32_t layer, cons
   if (rc != DASC_OK) return rc;
   if (workspace_bytes < need || (need > 0 && !workspace)) return DASC_E_WORKSPACE;
   if (!dasc::refresh_wy_supported(shape->dk, shape->dv)) return DASC_E_UNSUPPORTED;
-  if (int64_t(n_req) * shape->n_heads > INT32_MAX) return DASC_E_INVAL;
+  if (2 * int64_t(n_req) * shape->n_heads > INT32_MAX) return DASC_E_INVAL;  // GDN: 2 blocks a head
   if (n_rows == 0) slice_rows = 1;  // nothing is read; keeps the divisor non-zero
   (void)hipGetLastError();
-  dasc::launch_restore_refresh_wy(shape->arch == DASC_ARCH_KDA, n_req, shape->n_heads,
-                                  shape->n_qk_heads, layer, shape->n_layers, ckpt, n_ckpt_slots,
-                                  src_slot, slice_rows, n_rows, inv_row, states, n_pool, dst_slot,
-                                  k, v, g, beta, W, init_mode == DASC_INIT_ZERO,
-                                  reinterpret_cast<hipStream_t>(stream));
+  // GDN heads take the scalar-gate kernel, as in dasc_refresh (DASC_REFRESH_KERNEL=wy
+  // selects the channel-wise one)
+  const char* pick = std::getenv("DASC_REFRESH_KERNEL");
+  const bool force_wy = pick && std::strcmp(pick, "wy") == 0;
+  if (shape->arch == DASC_ARCH_GDN && !force_wy)
+    dasc::launch_restore_refresh_wy_gdn(n_req, shape->n_heads, shape->n_qk_heads, layer,
+                                        shape->n_layers, ckpt, n_ckpt_slots, src_slot, slice_rows,
+                                        n_rows, inv_row, states, n_pool, dst_slot, k, v, g, beta,
+                                        W, init_mode == DASC_INIT_ZERO,
+                                        reinterpret_cast<hipStream_t>(stream));
+  else
+    dasc::launch_restore_refresh_wy(shape->arch == DASC_ARCH_KDA, n_req, shape->n_heads,
+                                    shape->n_qk_heads, layer, shape->n_layers, ckpt, n_ckpt_slots,
+                                    src_slot, slice_rows, n_rows, inv_row, states, n_pool,
+                                    dst_slot, k, v, g, beta, W, init_mode == DASC_INIT_ZERO,
+                                    reinterpret_cast<hipStream_t>(stream));
   return dasc::launch_status();
 }

@@ -31,4 +31,12 @@ void launch_restore_refresh_wy(bool per_channel, int n_req, int H, int Hqk, int 
                                const uint16_t* k, const uint16_t* v, const float* g,
                                const float* beta, int W, int init_zero, hipStream_t st);
 
+// The scalar-gate GDN kernel's fused variant (dk = dv = 128).
+void launch_restore_refresh_wy_gdn(int n_req, int H, int Hqk, int layer, int L, const float* ckpt,
+                                   int64_t n_ckpt_slots, const int32_t* ck_slot,
+                                   int64_t slice_rows, int64_t n_rows, const int32_t* inv_row,
+                                   float* states, int64_t n_pool, const int32_t* slot,
+                                   const uint16_t* k, const uint16_t* v, const float* g,
+                                   const float* beta, int W, int init_zero, hipStream_t st);
+
 }  // namespace dasc

@@ -147,11 +147,7 @@ __device__ inline bf16x8 cat(bf16x4 a, bf16x4 b) {
 }
 
 // Packed checkpoint of the fused variant (unused when FUSED is false).
-struct CkptView {
-  const float* ckpt;
-  int64_t n_slots, slice_rows, n_rows;
-  const int32_t* slot;   // checkpoint slot per request
-};
+using dasc::CkptView;
 
 template <bool PER_CHANNEL, bool FUSED>
 __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
@@ -196,16 +192,11 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   // (kOmitted for an omitted row, kNoRow for an index outside the packed rows, which
   // restores as +0.0).  One thread per row fills the table in the A buffer, which is
   // free until the first chunk.
-  constexpr int64_t kOmitted = -1, kNoRow = -2;
+  using dasc::kOmitted;
   int64_t* sOff = reinterpret_cast<int64_t*>(smem + OFF_A);
   static_assert(D * 8 <= C * C * 4, "row table must fit in the A buffer");
   if (FUSED) {
-    if (tid < D) {
-      const int64_t p = inv_row[head_row + tid];
-      sOff[tid] = p < 0 ? kOmitted
-                : p >= ck.n_rows ? kNoRow
-                : dasc::slice_row(p, ck.slice_rows, ck.n_rows, ck.n_slots, cslot) * D;
-    }
+    if (tid < D) sOff[tid] = dasc::ckpt_row_offset(inv_row[head_row + tid], ck, cslot, D);
     __syncthreads();
   }
   if (FUSED && !any_omitted) {   // nothing to replay: restore the head as it is

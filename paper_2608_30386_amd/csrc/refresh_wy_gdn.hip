@@ -33,6 +33,7 @@
 
 #include <cstdint>
 
+#include "ckpt_layout.h"
 #include "refresh_kernels.h"
 
 namespace {
@@ -124,11 +125,15 @@ __device__ inline int xcd_major(int b, int n_blocks) {
   return (b & 7) * (n_blocks >> 3) + (b >> 3);
 }
 
+// FUSED: the initial state comes from the packed checkpoint (kept rows from their
+// packed position, written back to the pool at once; omitted rows +0.0) and every row
+// of the layer is written, as the channel-wise kernel's fused variant does.
+template <bool FUSED>
 __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     int H, int Hqk, int layer, int L, const int32_t* __restrict__ inv_row,
     float* __restrict__ states, int64_t n_pool, const int32_t* __restrict__ slot,
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, const float* __restrict__ g,
-    const float* __restrict__ beta, int W, int init_zero) {
+    const float* __restrict__ beta, int W, int init_zero, dasc::CkptView ck) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
   float* sT = reinterpret_cast<float*>(smem + OFF_T);
   __bf16* sTPH = reinterpret_cast<__bf16*>(smem + OFF_TPH);
@@ -154,19 +159,53 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
   const int64_t head_row = (int64_t(layer) * H + h) * D;
   bool mine = false;
   if (tid < D) mine = inv_row[head_row + tid] < 0;
-  if (!__syncthreads_or(mine)) return;
+  const bool any_omitted = __syncthreads_or(mine);
+  if (!FUSED && !any_omitted) return;
   const int64_t sl = slot[n];
   if (sl < 0 || sl >= n_pool) return;
   float* S_head = states + (sl * L * H * D + head_row) * D;
   const int col = DH * half + 16 * w + r;   // this lane's value column
+  int64_t cslot = 0;
+  if (FUSED) {
+    cslot = ck.slot[n];
+    if (cslot < 0 || cslot >= ck.n_slots) return;
+  }
+  // Fused: the head's checkpoint row table (float offsets, or dasc::kOmitted /
+  // dasc::kNoRow), in buffer 1's A tile, which the pipeline first writes two barriers
+  // after the initial state has been read.
+  int64_t* sOff = reinterpret_cast<int64_t*>(smem + BUF + B_A);
+  static_assert(D * 8 <= C * C * 4, "row table must fit in an A tile");
+  if (FUSED) {
+    if (tid < D) sOff[tid] = dasc::ckpt_row_offset(inv_row[head_row + tid], ck, cslot, D);
+    __syncthreads();
+  }
+  if (FUSED && !any_omitted) {   // nothing to replay: restore this half of the columns
+    for (int e = tid; e < D * DH / 4; e += 256) {
+      const int c = e / (DH / 4), v4 = e % (DH / 4);
+      const int64_t o = sOff[c];
+      const f32x4 val = o >= 0 ? reinterpret_cast<const f32x4*>(ck.ckpt + o + DH * half)[v4]
+                               : f32x4{0.f, 0.f, 0.f, 0.f};
+      reinterpret_cast<f32x4*>(S_head + int64_t(c) * D + DH * half)[v4] = val;
+    }
+    return;
+  }
 
   // S'[c][col] for c = 16 mt + 4q + i
   f32x4 S[8];
 #pragma unroll
   for (int mt = 0; mt < 8; ++mt)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      S[mt][i] = init_zero ? 0.f : S_head[int64_t(16 * mt + 4 * q + i) * D + col];
+    for (int i = 0; i < 4; ++i) {
+      const int c = 16 * mt + 4 * q + i;
+      if (FUSED) {
+        const int64_t o = sOff[c];
+        const float val = o >= 0 ? ck.ckpt[o + col] : 0.f;
+        S[mt][i] = init_zero ? 0.f : val;
+        if (o != dasc::kOmitted) S_head[int64_t(c) * D + col] = val;
+      } else {
+        S[mt][i] = init_zero ? 0.f : S_head[int64_t(c) * D + col];
+      }
+    }
 
   const int hk = h / (H / Hqk);
   const uint16_t* kp = k + (int64_t(n) * Hqk + hk) * W * D;
@@ -448,8 +487,21 @@ void launch_refresh_wy_gdn(int n_req, int H, int Hqk, int layer, int L, const in
                            const uint16_t* v, const float* g, const float* beta, int W,
                            int init_zero, hipStream_t st) {
   const dim3 grid(unsigned(n_req) * unsigned(H) * 2u), block(256);
-  hipLaunchKernelGGL(refresh_wy_gdn_kernel, grid, block, 0, st, H, Hqk, layer, L, inv_row, states,
-                     n_pool, slot, k, v, g, beta, W, init_zero);
+  const CkptView none{nullptr, 1, 1, 0, nullptr};
+  hipLaunchKernelGGL(refresh_wy_gdn_kernel<false>, grid, block, 0, st, H, Hqk, layer, L, inv_row,
+                     states, n_pool, slot, k, v, g, beta, W, init_zero, none);
+}
+
+void launch_restore_refresh_wy_gdn(int n_req, int H, int Hqk, int layer, int L, const float* ckpt,
+                                   int64_t n_ckpt_slots, const int32_t* ck_slot,
+                                   int64_t slice_rows, int64_t n_rows, const int32_t* inv_row,
+                                   float* states, int64_t n_pool, const int32_t* slot,
+                                   const uint16_t* k, const uint16_t* v, const float* g,
+                                   const float* beta, int W, int init_zero, hipStream_t st) {
+  const dim3 grid(unsigned(n_req) * unsigned(H) * 2u), block(256);
+  const CkptView ck{ckpt, n_ckpt_slots, slice_rows, n_rows, ck_slot};
+  hipLaunchKernelGGL(refresh_wy_gdn_kernel<true>, grid, block, 0, st, H, Hqk, layer, L, inv_row,
+                     states, n_pool, slot, k, v, g, beta, W, init_zero, ck);
 }
 
 }  // namespace dasc

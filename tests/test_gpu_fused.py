@@ -1,5 +1,6 @@
 """GPU parity of dasc_restore_refresh: one launch that restores a layer from its packed
-checkpoint and refreshes the omitted units.  Checked against the oracle's restore
+checkpoint and refreshes the omitted units (KDA rows on the channel-wise kernel, GDN heads
+on the scalar-gate kernel).  Checked against the oracle's restore
 followed by its refresh (refreshed rows within 2e-3, every other row of the layer
 bit-exact), bit for bit against the library's own dasc_restore + dasc_refresh, and for
 rows it must not touch (other layers, other pool slots)."""
@@ -119,12 +120,14 @@ def test_kimi_layer_fused(W):
     announce(f"kimi_layer fused W={W} sampled max rel err {err:.2e}, bit-equal to unfused")
 
 
-@pytest.mark.parametrize("init", ["restored", "zero"])
-def test_sliced_checkpoint_multilayer_kda(init):
+@pytest.mark.parametrize("arch,init", [("kda", "restored"), ("kda", "zero"), ("gdn", "restored"),
+                                       ("gdn", "zero")])
+def test_sliced_checkpoint_multilayer(arch, init):
     rng = np.random.default_rng(11)
     L, H, Hqk, W, n_req, T = 3, 4, 2, 100, 3, 3
-    sh = D.Shape("kda", L, H, Hqk, 128, 128)
-    g_static = D.dasc_static_log_decay(rng.uniform(math.log(1e-4), 0, size=(L, H, 128)))
+    sh = D.Shape(arch, L, H, Hqk, 128, 128)
+    unit_shape = (L, H, 128) if arch == "kda" else (L, H)   # KDA: rows; GDN: heads
+    g_static = D.dasc_static_log_decay(rng.uniform(math.log(1e-4), 0, size=unit_shape))
     g_static[1, 0] = math.log(1e-3) / 2.0          # layer 1, head 0: every row omitted
     g_static[1, 1] = math.log(1e-3) / 1e4          # layer 1, head 1: every row kept
     plan = D.dasc_plan(sh, g_static, "threshold", 0, 64, T)
@@ -137,7 +140,7 @@ def test_sliced_checkpoint_multilayer_kda(init):
     n_pool = 6
     dst = [5, 1, 3]
     pool = sentinel_pool(n_pool, sh)
-    inp = _inputs_128("kda", n_req, H, Hqk, W, seed=5)
+    inp = _inputs_128(arch, n_req, H, Hqk, W, seed=5)
     got = run_fused(sh, 1, ck, ck_slots, plan["inv_row"], pool, dst, inp, W, R, T, C, init)
     pairs = [(n, h) for n in range(n_req) for h in range(H)]
     err = check_fused(sh, 1, got, restored, plan["inv_row"], dst, inp, pairs, init, n_pool)
@@ -146,7 +149,7 @@ def test_sliced_checkpoint_multilayer_kda(init):
     g = got.reshape(n_pool, -1, 128).view(np.uint32)[:, lo:hi]
     r = ref.reshape(n_pool, -1, 128).view(np.uint32)[:, lo:hi]
     assert np.array_equal(g[dst], r[dst]), "fused differs from restore + refresh"
-    announce(f"sliced T={T} kda fused init={init} max rel err {err:.2e}")
+    announce(f"sliced T={T} {arch} fused init={init} max rel err {err:.2e}")
 
 
 def test_qwen_gdn_fused_one_layer():
@@ -167,4 +170,9 @@ def test_qwen_gdn_fused_one_layer():
     om = (lib["inv_row"][lo:lo + sh.n_heads * sh.dk] < 0).reshape(sh.n_heads, sh.dk)
     pairs = sample_pairs(n_req, sh.n_heads, om, 6, seed=layer)
     err = check_fused(sh, layer, got, restored, lib["inv_row"], dst, inp, pairs, "restored", n_pool)
-    announce(f"qwen_gdn fused layer={layer} sampled max rel err {err:.2e}")
+    ref = run_unfused(sh, layer, ck, ck_slots, lib["inv_row"], pool, dst, inp, 1024, R, 1, R)
+    hi = lo + sh.n_heads * sh.dk
+    g_ = got.reshape(n_pool, -1, sh.dv).view(np.uint32)[:, lo:hi]
+    r_ = ref.reshape(n_pool, -1, sh.dv).view(np.uint32)[:, lo:hi]
+    assert np.array_equal(g_[dst], r_[dst]), "fused differs from restore + refresh"
+    announce(f"qwen_gdn fused layer={layer} sampled max rel err {err:.2e}, bit-equal to unfused")
