@@ -21,8 +21,9 @@
 // A): with b = n mod 2,
 //   P1  wave 0 inverts the diagonal blocks of I + A(n); waves 1-3 form X(n) on their
 //       columns and stage chunk n+1 into buffer b^1 (wave 1 also sums its gates);
-//   P2  wave 0 forms X(n); wave 1 forms T10(n) and T'(n); waves 2-3 write the rest of
-//       T'(n) and the A tiles of chunk n+1; waves 1-3 issue the loads of chunk n+2;
+//   P2  wave 0 forms X(n) and one A tile of chunk n+1; wave 1 forms T10(n) and T'(n);
+//       waves 2-3 write the rest of T'(n) and the other two A tiles of chunk n+1;
+//       waves 1-3 issue the loads of chunk n+2;
 //   P3  every wave forms U(n) and updates its columns of S'.
 // Three barriers a chunk; the serial inversion runs beside the staging and X.  Register
 // chaining, operand splitting, padded LDS rows and the buffer-resource loads (tokens
@@ -71,6 +72,25 @@ constexpr int LDS_BYTES = OFF_TPL + C * SP * 2;
 static_assert(BUF % 16 == 0 && LDS_BYTES <= 81920, "two blocks per CU");
 
 __device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// One DPP move: lane l takes v from the lane CTRL selects within its row of 16 (0 where
+// that lane is outside the row); rows outside ROW_MASK keep 0.
+template <int CTRL, int ROW_MASK>
+__device__ inline float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL,
+                                                               ROW_MASK, 0xF, true));
+}
+
+// Inclusive prefix sum over lanes 0..31: shifts by 1, 2, 4, 8 within each row of 16
+// lanes, then row 1 adds the last lane of row 0 (row_bcast:15).  No LDS round trips.
+__device__ inline float scan32(float x) {
+  x += dpp<0x111, 0xF>(x);   // row_shr:1
+  x += dpp<0x112, 0xF>(x);   // row_shr:2
+  x += dpp<0x114, 0xF>(x);   // row_shr:4
+  x += dpp<0x118, 0xF>(x);   // row_shr:8
+  x += dpp<0x142, 0xA>(x);   // row_bcast:15 into rows 1 and 3
+  return x;
+}
 
 __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* p, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
@@ -217,8 +237,9 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
 
   // Waves 1-3 (192 threads, index st = tid - 64) load and stage a chunk:
   //   keys row-major: 8-channel units u = st + 192 i (< 512): token u / 16, channels 8 (u % 16);
-  //   keys transposed: items p = st + 192 i (< 256): channels 2 (p % 64), +1, tokens 8 (p / 64) .. +7;
+  //   keys transposed: items p (< 256): channels 2 (p % 64), +1, tokens 8 (p / 64) .. +7;
   //   values: items p (< 256): columns 64 half + 2 (p % 32), +1, tokens 4 (p / 32) .. +3;
+  //     item p = st for every wave and, on wave 3, also 192 + lane (wave 1 sums the gates);
   //   gate and beta: token st % 32 (wave 1 sums them).
   const int st = tid - 64;
   uint4 kraw[3];
@@ -234,7 +255,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int p = st + 192 * i;
+      const int p = i == 0 ? st : (w == 3 ? 192 + lane : 256);
       if (p < 256) {
 #pragma unroll
         for (int j = 0; j < 8; ++j)
@@ -260,7 +281,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int p = st + 192 * i;
+      const int p = i == 0 ? st : (w == 3 ? 192 + lane : 256);
       if (p < 256) {
         uint32_t lo[4], hi[4];
 #pragma unroll
@@ -280,14 +301,9 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
         *reinterpret_cast<uint2*>(sVT + (v2 + 1) * SV + t4) = make_uint2(vhi0, vhi1);
       }
     }
-    if (w == 1) {   // inclusive running sum of the log2 gates by lane shuffles
-      float x = lane < C ? fmaxf(graw, kGateFloor) * kLog2e : 0.f;
-#pragma unroll
-      for (int d = 1; d < C; d <<= 1) {
-        const float y = __shfl_up(x, d);
-        if (lane >= d) x += y;
-      }
-      const float gc = __shfl(x, C - 1);
+    if (w == 1) {   // inclusive running sum of the log2 gates over lanes 0..31
+      const float x = scan32(lane < C ? fmaxf(graw, kGateFloor) * kLog2e : 0.f);
+      const float gc = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), C - 1));
       if (lane < C) {
         bG(b)[lane] = x;
         bEG(b)[lane] = ex2(x);
@@ -296,17 +312,13 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       }
     }
   };
-  // A of the chunk in buffer b, strictly lower, tiles (0,0), (1,0), (1,1): wave 2 takes
-  // the first two, wave 3 the third
-  auto a_tiles = [&](int b) {
+  // A of the chunk in buffer b, strictly lower, tile (0,0), (1,0) or (1,1)
+  auto a_tile = [&](int b, int tile) {
     const uint16_t* sK = bK(b);
     const float* sG = bG(b);
     const float* sBeta = bBeta(b);
     float* sA = bA(b);
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      const int tile = w == 2 ? tt : 2;
-      if (w == 3 && tt == 1) break;
+    {
       const int ti = tile == 0 ? 0 : 1, si = tile == 2 ? 1 : 0;
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -352,7 +364,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
   if (w > 0) fetch(0);
   if (w > 0) stage(0);
   __syncthreads();
-  if (w >= 2) a_tiles(0);
+  if (w != 1) a_tile(0, w == 0 ? 0 : w - 1);
   if (w > 0) fetch(C);
   __syncthreads();
 
@@ -387,6 +399,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       const float* sBeta = bBeta(b);
       if (w == 0) {
         form_x(b, X);
+        if (more) a_tile(b ^ 1, 0);   // the next chunk's A: tile (0,0) here, the others on waves 2-3
       } else if (w == 1) {
         f32x4 y = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -419,7 +432,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
           sTPH[t * SP + s] = a;
           sTPL[t * SP + s] = bb;
         }
-        if (w >= 2 && more) a_tiles(b ^ 1);
+        if (w >= 2 && more) a_tile(b ^ 1, w - 1);
         if (t0 + 2 * C < W) fetch(t0 + 2 * C);
       }
     }
