@@ -56,14 +56,11 @@
 
 #include "ckpt_layout.h"
 #include "refresh_kernels.h"
+#include "wy_ops.h"
 
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
+using namespace dasc_wy;
 
 constexpr int C = 32;       // tokens per chunk
 constexpr int D = 128;      // dk = dv
@@ -73,7 +70,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 // padded row strides (elements)
 constexpr int SG = 132;     // f32 [C][SG]   cumulative log2-decay
 constexpr int SK = 136;     // bf16 [C][SK]  keys, K_G
-constexpr int SV = 40;      // bf16 [D][SV]  values transposed, K_H^T
+constexpr int SV = 40;      // bf16 [D][SV]  K_H^T
 constexpr int SP = 36;      // bf16 [C][SP]  T' (8-byte aligned rows)
 
 // LDS map (bytes).  The key buffer is dead once A and K_H are built and then holds
@@ -95,56 +92,6 @@ static_assert(C * C * 4 + 2 * C * SP * 2 <= C * SK * 2, "T and T' must fit in th
 static_assert(LDS_BYTES <= 81920, "two blocks per CU");
 
 __device__ inline float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
-
-// Raw buffer resource over exactly `bytes` bytes: a load whose total offset (vector +
-// scalar + immediate) reaches past the end returns zero instead of touching memory.
-// Tokens past the window therefore arrive as k = v = 0, g = 0, beta = 0, which are
-// identity steps of the recurrence, and no load needs a clamp or a mask.
-__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* p, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
-}
-__device__ inline float ldf(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
-}
-__device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-__device__ inline void split(float x, __bf16& hi, __bf16& lo) {
-  hi = static_cast<__bf16>(x);
-  lo = static_cast<__bf16>(x - static_cast<float>(hi));
-}
-
-// Eight values split at once: two values per packed conversion (3 VALU per value).
-__device__ inline void split8(const float* x, bf16x8& hi, bf16x8& lo) {
-  uint32_t h[4], l[4];
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const uint32_t hw = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x[2 * p], x[2 * p + 1]}, bf16x2));
-    const float r0 = __uint_as_float(hw << 16), r1 = __uint_as_float(hw & 0xFFFF0000u);
-    h[p] = hw;
-    l[p] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x[2 * p] - r0, x[2 * p + 1] - r1}, bf16x2));
-  }
-  hi = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
-  lo = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
-}
-
-__device__ inline f32x4 mma(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
-// a b with both operands split: a_lo b_hi + a_hi b_lo + a_hi b_hi (small terms first)
-__device__ inline f32x4 mma3(bf16x8 ah, bf16x8 al, bf16x8 bh, bf16x8 bl, f32x4 c) {
-  c = mma(al, bh, c);
-  c = mma(ah, bl, c);
-  return mma(ah, bh, c);
-}
-
-__device__ inline f32x4 mma32(float a, float b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
-__device__ inline bf16x8 cat(bf16x4 a, bf16x4 b) {
-  return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-}
 
 // Packed checkpoint of the fused variant (unused when FUSED is false).
 using dasc::CkptView;
@@ -398,7 +345,8 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     // the next chunk's inputs load while this chunk finishes
     fetch(t0 + C);   // past the window this reads zeros
     __syncthreads();
-    // T' = T Diag(beta), split hi/lo.  Wave 1 forms the off-diagonal block
+    // -T' = -T Diag(beta), split hi/lo (stored negated so that U takes X - V, which one
+    // dot2 per value forms from the packed values).  Wave 1 forms the off-diagonal block
     // T10 = -T11 (A10 T00) on fp32 MFMA, the product staying in registers between the
     // two steps; the other waves write the diagonal blocks and the zero upper block.
     if (w == 1) {
@@ -414,7 +362,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       for (int i = 0; i < 4; ++i) {
         const int t = 16 + 4 * q + i;
         __bf16 a, b;
-        split(-z[i] * br, a, b);
+        split(z[i] * br, a, b);   // -T'10
         sTPH[t * SP + r] = a;
         sTPL[t * SP + r] = b;
       }
@@ -429,7 +377,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         {
           const float val = s <= t ? sT[t * C + s] * sBeta[s] : 0.f;
           __bf16 a, b;
-          split(val, a, b);
+          split(-val, a, b);
           sTPH[t * SP + s] = a;
           sTPL[t * SP + s] = b;
         }
@@ -463,7 +411,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 
     __syncthreads();   // T' complete
 
-    // ---- U = T' (V - X): the difference stays in registers as the B operand --------
+    // ---- U = (-T')(X - V): the difference stays in registers as the B operand ------
     f32x4 U[2][2];
     {
       bf16x8 yh[2], yl[2];
@@ -474,8 +422,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         for (int mu = 0; mu < 2; ++mu)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const uint32_t vv = vreg[mu][i];
-            x[4 * mu + i] = __uint_as_float(nt ? (vv & 0xFFFF0000u) : (vv << 16)) - X[mu][nt][i];
+            x[4 * mu + i] = dot2(as_bf2(vreg[mu][i]), nt ? kNegHi : kNegLo, X[mu][nt][i]);
           }
         split8(x, yh[nt], yl[nt]);
       }

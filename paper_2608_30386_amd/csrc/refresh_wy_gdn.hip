@@ -36,14 +36,11 @@
 
 #include "ckpt_layout.h"
 #include "refresh_kernels.h"
+#include "wy_ops.h"
 
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
+using namespace dasc_wy;
 
 constexpr int C = 32;       // tokens per chunk
 constexpr int D = 128;      // dk = dv
@@ -71,8 +68,6 @@ constexpr int OFF_TPL = OFF_TPH + C * SP * 2;
 constexpr int LDS_BYTES = OFF_TPL + C * SP * 2;
 static_assert(BUF % 16 == 0 && LDS_BYTES <= 81920, "two blocks per CU");
 
-__device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
-
 // One DPP move: lane l takes v from the lane CTRL selects within its row of 16 (0 where
 // that lane is outside the row); rows outside ROW_MASK keep 0.
 template <int CTRL, int ROW_MASK>
@@ -90,50 +85,6 @@ __device__ inline float scan32(float x) {
   x += dpp<0x118, 0xF>(x);   // row_shr:8
   x += dpp<0x142, 0xA>(x);   // row_bcast:15 into rows 1 and 3
   return x;
-}
-
-__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* p, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, bytes, 0x00020000);
-}
-__device__ inline float ldf(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
-}
-
-__device__ inline void split(float x, __bf16& hi, __bf16& lo) {
-  hi = static_cast<__bf16>(x);
-  lo = static_cast<__bf16>(x - static_cast<float>(hi));
-}
-
-// Eight values split at once: two values per packed conversion.
-__device__ inline void split8(const float* x, bf16x8& hi, bf16x8& lo) {
-  uint32_t h[4], l[4];
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const uint32_t hw = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x[2 * p], x[2 * p + 1]}, bf16x2));
-    const float r0 = __uint_as_float(hw << 16), r1 = __uint_as_float(hw & 0xFFFF0000u);
-    h[p] = hw;
-    l[p] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x[2 * p] - r0, x[2 * p + 1] - r1}, bf16x2));
-  }
-  hi = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
-  lo = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
-}
-
-__device__ inline f32x4 mma(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
-__device__ inline f32x4 mma32(float a, float b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
-__device__ inline bf16x8 cat(bf16x4 a, bf16x4 b) {
-  return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-}
-
-// Row-major bf16 operand with the contraction index k(q, e) (four values at p, four at
-// p + 16).
-__device__ inline bf16x8 ld_op(const __bf16* p) {
-  return cat(*reinterpret_cast<const bf16x4*>(p), *reinterpret_cast<const bf16x4*>(p + 16));
 }
 
 // Blocks are dealt to the eight XCDs in turn (block b starts on XCD b mod 8).  Renumber
@@ -392,7 +343,8 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     }
     __syncthreads();
 
-    // ---- P2: X (wave 0) | T' = T Diag(beta) split, T10 = -T11 (A10 T00) on wave 1 |
+    // ---- P2: X (wave 0) | -T' = -T Diag(beta) split (negated so that U takes X - V, one
+    //          dot2 per value), T10 = -T11 (A10 T00) on wave 1 |
     //          the next chunk's A tiles (waves 2-3) | loads of the chunk after next
     {
       const float* sA = bA(b);
@@ -413,7 +365,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
         for (int i = 0; i < 4; ++i) {
           const int t = 16 + 4 * q + i;
           __bf16 a, bb;
-          split(-z[i] * br, a, bb);
+          split(z[i] * br, a, bb);   // -T'10
           sTPH[t * SP + r] = a;
           sTPL[t * SP + r] = bb;
         }
@@ -428,7 +380,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
           const int s = e < 512 ? e & 31 : 16 + ((e - 512) & 15);
           const float val = s <= t ? sT[t * C + s] * sBeta[s] : 0.f;
           __bf16 a, bb;
-          split(val, a, bb);
+          split(-val, a, bb);
           sTPH[t * SP + s] = a;
           sTPL[t * SP + s] = bb;
         }
@@ -438,7 +390,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     }
     __syncthreads();
 
-    // ---- P3: U = T' (V - X), Diag(2^{G_C - G}) U, S' <- 2^{G_C} S' + K^T U --------------
+    // ---- P3: U = (-T')(X - V), Diag(2^{G_C - G}) U, S' <- 2^{G_C} S' + K^T U ----------
     {
       const uint16_t* sVT = bVT(b);
       const float* sEH = bEH(b);
@@ -448,10 +400,9 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
 #pragma unroll
       for (int mu = 0; mu < 2; ++mu) {
         const uint2 vv = *reinterpret_cast<const uint2*>(sVT + (16 * w + r) * SV + 16 * mu + 4 * q);
-        const float vf[4] = {__uint_as_float(vv.x << 16), __uint_as_float(vv.x & 0xFFFF0000u),
-                             __uint_as_float(vv.y << 16), __uint_as_float(vv.y & 0xFFFF0000u)};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) x[4 * mu + i] = vf[i] - X[mu][i];
+        for (int i = 0; i < 4; ++i)
+          x[4 * mu + i] = dot2(as_bf2(i < 2 ? vv.x : vv.y), (i & 1) ? kNegHi : kNegLo, X[mu][i]);
       }
       split8(x, yh, yl);
 #pragma unroll
