@@ -469,11 +469,14 @@ def bench_gdn(torch, args):
         inp = refresh_inputs(wl, W, lam[l], salt=l)
         layers.append((_bf16(torch, inp["k"]), _bf16(torch, inp["v"]),
                        torch.from_numpy(inp["g"]).cuda(), torch.from_numpy(inp["beta"]).cuda()))
+    # the per-chunk WY factors of the two-launch GDN kernel, allocated once
+    ws = torch.empty(D.dasc_refresh_workspace_bytes(sh, wl.n_req, W), dtype=torch.uint8,
+                     device="cuda")
     timer = KernelTimer(torch)
 
     def ref():
         for l, (k, v, g, b) in enumerate(layers):
-            D.dasc_refresh(sh, l, inv_row, active, req, k, v, g, b, W)
+            D.dasc_refresh(sh, l, inv_row, active, req, k, v, g, b, W, workspace=ws)
 
     def plain_step():
         D.dasc_pack(sh, states, ids, unit_row, ckpt, ids)
@@ -503,7 +506,8 @@ def bench_gdn(torch, args):
 
         def fused():
             for l, (k, v, g, b) in enumerate(layers):
-                D.dasc_restore_refresh(sh, l, ckpt, req, inv_row, active, req, k, v, g, b, W, n_rows=R)
+                D.dasc_restore_refresh(sh, l, ckpt, req, inv_row, active, req, k, v, g, b, W, n_rows=R,
+                                       workspace=ws)
         timer.run("restore_refresh", fused)
 
     load_wr()
@@ -549,8 +553,8 @@ def bench_gdn(torch, args):
         "kernels": {"pack": {"ms": t["pack"], "GBps": bp / t["pack"] / 1e6},
                     "restore": {"ms": t["restore"], "GBps": br / t["restore"] / 1e6},
                     "refresh_all_layers": {"ms": t["refresh_all_layers"], "GBps": ach,
-                                           "launches": wl.n_layers, "bytes": bytes_ref},
-                    "restore_refresh_fused": {"ms": t["restore_refresh"], "launches": wl.n_layers,
+                                           "launches": 2 * wl.n_layers, "bytes": bytes_ref},
+                    "restore_refresh_fused": {"ms": t["restore_refresh"], "launches": 2 * wl.n_layers,
                                               "unfused_ms": t["restore_req"] + t["refresh_req"],
                                               "requests": wl.n_req}},
         "plan_host_ms": plan_s * 1e3,

@@ -272,7 +272,12 @@ int dasc_restore_q8(const dasc_shape *shape, const int8_t *q, const float *scale
 
 /* ---- Load with refresh: bounded-suffix replay (Sec. 4.2 DASC-WR, Eq. 1) --- */
 
-/* Device workspace dasc_refresh needs for n_req requests and window W (may be 0).
+/* Device workspace dasc_refresh and dasc_restore_refresh need for n_req requests and
+ * window W.  GDN heads at dk = dv = 128 hold the state-independent factor of every
+ * 32-token chunk there (the chunk's (I + A)^{-1} Diag(beta) of the WY form of Eq. 1,
+ * split into two bf16 words per entry) between the two launches of their kernel:
+ * n_req * n_heads * ceil(W / 32) * 4096 bytes.  Every other shape needs 0.  The caller
+ * owns it; its contents need not be initialised and are dead after the call.
  * Errors: DASC_E_INVAL (NULL shape/bytes, n_req < 1, W < 1), DASC_E_SHAPE. */
 int dasc_refresh_workspace_bytes(const dasc_shape *shape, int32_t n_req, int32_t W,
                                  size_t *bytes);
@@ -293,7 +298,8 @@ int dasc_refresh_workspace_bytes(const dasc_shape *shape, int32_t n_req, int32_t
  *   v:    device bf16 bits [n_req, H,   W, dv]   (16-byte aligned)
  *   g:    device fp32 log-gates, [n_req, H, W, dk] (KDA) or [n_req, H, W] (GDN)
  *   beta: device fp32 [n_req, H, W]
- *   workspace: device, at least dasc_refresh_workspace_bytes (may be NULL if that is 0).
+ *   workspace: device, at least dasc_refresh_workspace_bytes, 16-byte aligned (may be
+ *              NULL if that is 0); overlapping calls must not share one.
  * Arithmetic is fp32 with bf16 inputs widened exactly.
  * Errors: DASC_E_INVAL (NULL pointer, misalignment, layer out of [0, L), n_req < 1,
  * W < 1 or W > DASC_MAX_WINDOW, bad init_mode, n_pool < 1), DASC_E_SHAPE (bad shape),

@@ -114,13 +114,23 @@ void launch_column(bool per_channel, dim3 grid, dim3 block, size_t lds, hipStrea
                        L, inv_row, states, n_pool, slot, k, v, g, beta, W, init_zero);
 }
 
+// Does this shape take the two-launch scalar-gate GDN kernel (unless the channel-wise
+// kernel is forced with DASC_REFRESH_KERNEL)?
+bool uses_gdn_factors(const dasc_shape* shape) {
+  return shape->arch == DASC_ARCH_GDN && dasc::refresh_wy_supported(shape->dk, shape->dv);
+}
+
 }  // namespace
 
 extern "C" int dasc_refresh_workspace_bytes(const dasc_shape* shape, int32_t n_req, int32_t W,
                                             size_t* bytes) {
   if (!shape || !bytes || n_req < 1 || W < 1) return DASC_E_INVAL;
   if (!dasc::valid_shape(shape)) return DASC_E_SHAPE;
-  *bytes = 0;
+  // GDN heads at dk = dv = 128 keep each chunk's WY factor -T' between the two launches
+  // of their kernel; every other path needs nothing.
+  *bytes = uses_gdn_factors(shape)
+               ? dasc::gdn_factor_workspace_bytes(n_req, shape->n_heads, W)
+               : 0;
   return DASC_OK;
 }
 
@@ -141,6 +151,7 @@ extern "C" int dasc_refresh(const dasc_shape* shape, int32_t layer, const int32_
   int rc = dasc_refresh_workspace_bytes(shape, n_req, W, &need);
   if (rc != DASC_OK) return rc;
   if (workspace_bytes < need || (need > 0 && !workspace)) return DASC_E_WORKSPACE;
+  if (need > 0 && !dasc::aligned16(workspace)) return DASC_E_INVAL;
   const int dk = shape->dk, dv = shape->dv;
   if (dv > 256) return DASC_E_UNSUPPORTED;
   if (2 * int64_t(n_req) * shape->n_heads > INT32_MAX) return DASC_E_INVAL;  // GDN: 2 blocks a head
@@ -159,10 +170,11 @@ extern "C" int dasc_refresh(const dasc_shape* shape, int32_t layer, const int32_
   const char* pick = std::getenv("DASC_REFRESH_KERNEL");
   const bool force_column = pick && std::strcmp(pick, "column") == 0;
   const bool force_wy = pick && std::strcmp(pick, "wy") == 0;
-  if (!force_column && !force_wy && !per_channel && dasc::refresh_wy_supported(dk, dv)) {
+  if (!force_column && !force_wy && uses_gdn_factors(shape)) {
+    if (dasc::gdn_factor_blocks(n_req, shape->n_heads, W) > INT32_MAX) return DASC_E_INVAL;
     dasc::launch_refresh_wy_gdn(n_req, shape->n_heads, shape->n_qk_heads, layer,
                                 shape->n_layers, inv_row, states, n_pool, slot, k, v, g, beta, W,
-                                zero, st);
+                                zero, workspace, st);
     return dasc::launch_status();
   }
   if (!force_column && dasc::refresh_wy_supported(dk, dv)) {
@@ -213,6 +225,7 @@ extern "C" int dasc_restore_refresh(const dasc_shape* shape, int32_t layer, cons
   int rc = dasc_refresh_workspace_bytes(shape, n_req, W, &need);
   if (rc != DASC_OK) return rc;
   if (workspace_bytes < need || (need > 0 && !workspace)) return DASC_E_WORKSPACE;
+  if (need > 0 && !dasc::aligned16(workspace)) return DASC_E_INVAL;
   if (!dasc::refresh_wy_supported(shape->dk, shape->dv)) return DASC_E_UNSUPPORTED;
   if (2 * int64_t(n_req) * shape->n_heads > INT32_MAX) return DASC_E_INVAL;  // GDN: 2 blocks a head
   if (n_rows == 0) slice_rows = 1;  // nothing is read; keeps the divisor non-zero
@@ -221,13 +234,14 @@ extern "C" int dasc_restore_refresh(const dasc_shape* shape, int32_t layer, cons
   // selects the channel-wise one)
   const char* pick = std::getenv("DASC_REFRESH_KERNEL");
   const bool force_wy = pick && std::strcmp(pick, "wy") == 0;
-  if (shape->arch == DASC_ARCH_GDN && !force_wy)
+  if (uses_gdn_factors(shape) && !force_wy) {
+    if (dasc::gdn_factor_blocks(n_req, shape->n_heads, W) > INT32_MAX) return DASC_E_INVAL;
     dasc::launch_restore_refresh_wy_gdn(n_req, shape->n_heads, shape->n_qk_heads, layer,
                                         shape->n_layers, ckpt, n_ckpt_slots, src_slot, slice_rows,
                                         n_rows, inv_row, states, n_pool, dst_slot, k, v, g, beta,
-                                        W, init_mode == DASC_INIT_ZERO,
+                                        W, init_mode == DASC_INIT_ZERO, workspace,
                                         reinterpret_cast<hipStream_t>(stream));
-  else
+  } else
     dasc::launch_restore_refresh_wy(shape->arch == DASC_ARCH_KDA, n_req, shape->n_heads,
                                     shape->n_qk_heads, layer, shape->n_layers, ckpt, n_ckpt_slots,
                                     src_slot, slice_rows, n_rows, inv_row, states, n_pool,

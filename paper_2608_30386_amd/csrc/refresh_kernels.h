@@ -3,6 +3,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstddef>
 #include <cstdint>
 
 namespace dasc {
@@ -15,11 +16,16 @@ void launch_refresh_wy(bool per_channel, int n_req, int H, int Hqk, int layer, i
                        int W, int init_zero, hipStream_t st);
 
 // GDN heads (scalar gate per token), dk = dv = 128: keys enter the MFMAs exactly and
-// the decays stay outside the contractions; two blocks per head (value-column halves).
+// the decays stay outside the contractions.  Two launches: the per-chunk factor -T' of
+// every refreshed head into `ws`, then the state recurrence (two blocks per head, one per
+// value-column half) reading it.  `ws` holds gdn_factor_workspace_bytes(n_req, H, W).
+constexpr int kGdnFactorBytesPerChunk = 4096;
+size_t gdn_factor_workspace_bytes(int n_req, int H, int W);
+int64_t gdn_factor_blocks(int n_req, int H, int W);
 void launch_refresh_wy_gdn(int n_req, int H, int Hqk, int layer, int L, const int32_t* inv_row,
                            float* states, int64_t n_pool, const int32_t* slot, const uint16_t* k,
                            const uint16_t* v, const float* g, const float* beta, int W,
-                           int init_zero, hipStream_t st);
+                           int init_zero, void* ws, hipStream_t st);
 
 // The same kernel fused with the restore of the layer: the initial state of each head is
 // read from the packed checkpoint (kept rows; omitted rows start at zero) and every row
@@ -37,6 +43,7 @@ void launch_restore_refresh_wy_gdn(int n_req, int H, int Hqk, int layer, int L, 
                                    int64_t slice_rows, int64_t n_rows, const int32_t* inv_row,
                                    float* states, int64_t n_pool, const int32_t* slot,
                                    const uint16_t* k, const uint16_t* v, const float* g,
-                                   const float* beta, int W, int init_zero, hipStream_t st);
+                                   const float* beta, int W, int init_zero, void* ws,
+                                   hipStream_t st);
 
 }  // namespace dasc

@@ -1,34 +1,31 @@
 // Chunkwise WY-form refresh for GDN heads (one scalar gate per token), dk = dv = 128,
-// on bf16 MFMA (gfx950).
+// on bf16 MFMA (gfx950), in two launches.
 //
 // Same recurrence and chunk algebra as the channel-wise kernel (Sec. 3.1, Eq. 1 on
 // S' = S^T, chunks of C = 32 tokens, G_t = sum_{r<=t} g_r in log2 units), but with a
 // scalar decay per token every decay factor leaves the contractions:
 //     A_ts = beta_t (K K^T)_ts 2^{G_t - G_s}           (s < t)
+//     T'   = (I + A)^{-1} Diag(beta)
 //     X    = K_G S' = Diag(2^{G_t}) (K S')
 //     S'  <- 2^{G_C} S' + K^T (Diag(2^{G_C - G_t}) U),  U = T'(V - X)
 // Keys are bf16, so K is an exact MFMA operand: K K^T takes one bf16 pass (the products
 // are exact in fp32) and K S', K^T U take two (state and update split into bf16 hi + lo)
-// instead of three.  Only 32 exponentials per chunk remain, and no K_G / K_H tiles are
-// built.
+// instead of three.
 //
-// Work split: one 256-thread block per (request, head, half of the value columns); wave
-// w owns columns [64 half + 16 w, +16) of S' (128 x 16 fp32 in MFMA accumulators).  The
-// S-independent part (A, T, T') is recomputed by both halves; it is cheap here, and the
-// split doubles the blocks of a launch (a layer of a GDN model has few omitted heads).
+// A and T' do not depend on the state.  gdn_factor_kernel builds them for every chunk
+// of every refreshed head at once (one wave per chunk) and stores -T', split into bf16
+// hi + lo in the order the U contraction loads it, in the caller's workspace.  The
+// state recurrence, refresh_wy_gdn_kernel, then carries per chunk only X, U and the
+// update: its serial chain no longer holds the triangular solve, and it takes one
+// barrier a chunk.
 //
-// Software pipeline over chunks (two LDS buffers for a chunk's keys, values, gates and
-// A): with b = n mod 2,
-//   P1  wave 0 inverts the diagonal blocks of I + A(n); waves 1-3 form X(n) on their
-//       columns and stage chunk n+1 into buffer b^1 (wave 1 also sums its gates);
-//   P2  wave 0 forms X(n) and one A tile of chunk n+1; wave 1 forms T10(n) and T'(n);
-//       waves 2-3 write the rest of T'(n) and the other two A tiles of chunk n+1;
-//       waves 1-3 issue the loads of chunk n+2;
-//   P3  every wave forms U(n) and updates its columns of S'.
-// Three barriers a chunk; the serial inversion runs beside the staging and X.  Register
-// chaining, operand splitting, padded LDS rows and the buffer-resource loads (tokens
-// past the window read as zeros: identity steps) are as in the channel-wise kernel;
-// per-token log-gates are floored at -10 in the same way.
+// Recurrence work split: one 256-thread block per (request, head, half of the value
+// columns); wave w owns columns [64 half + 16 w, +16) of S' (128 x 16 fp32 in MFMA
+// accumulators).  Two LDS buffers alternate by chunk: while a chunk is contracted out of
+// one, the next is staged into the other from registers loaded a chunk earlier.
+// Register chaining, operand splitting, padded LDS rows and the buffer-resource loads
+// (tokens past the window read as zeros: identity steps) are as in the channel-wise
+// kernel; per-token log-gates are floored at -10 in the same way.
 
 #include <hip/hip_runtime.h>
 
@@ -48,24 +45,37 @@ constexpr int DH = 64;      // value columns per block
 constexpr float kGateFloor = -10.f;
 constexpr float kLog2e = 1.4426950408889634f;
 
+// -T' of one chunk in the workspace: [mu][hi/lo][lane][8 bf16], where lane (q, r) holds
+// row 16 mu + r at the register-chained contraction index k(q, e) -- one 16-byte load
+// per (mu, hi/lo) and lane.
+constexpr int TP_VEC = 2 * 2 * 64;   // uint4 per chunk (4 KiB)
+static_assert(TP_VEC * 16 == dasc::kGdnFactorBytesPerChunk, "factor size");
+
+// ---- factor kernel: per-wave LDS (padded f32 rows) ---------------------------------------
+// One tile holds A and then, in place, T = (I + A)^{-1}: the substitution overwrites the
+// diagonal blocks row by row after reading them, and T10 replaces A10 once A10 T00 is in
+// registers.
+constexpr int SA = 33;
+constexpr int F_M = 0;                       // f32 [C][SA]  A, then T
+constexpr int F_G = F_M + C * SA * 4;        // f32 [C]      G_t
+constexpr int F_B = F_G + C * 4;             // f32 [C]      beta_t
+constexpr int F_WAVE = F_B + C * 4;
+
+// The lanes of one wave see each other's LDS writes: the wave waits for its LDS accesses
+// to finish, and the compiler moves no memory access across the wait.
+__device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// ---- recurrence kernel: LDS, two buffers by chunk parity ---------------------------------
 constexpr int SK = 136;     // bf16 [C][SK]   keys, row-major
 constexpr int SV = 40;      // bf16 [D][SV]   keys transposed; [DH][SV] values transposed
-constexpr int SP = 36;      // bf16 [C][SP]   T'
-
-// LDS map (bytes): one buffer per chunk parity, then T and T' (single).
 constexpr int B_K = 0;                          // bf16 [C][SK]  keys
 constexpr int B_KT = B_K + C * SK * 2;          // bf16 [D][SV]  keys transposed
 constexpr int B_VT = B_KT + D * SV * 2;         // bf16 [DH][SV] this half's values transposed
-constexpr int B_A = B_VT + DH * SV * 2;         // f32  [C][C]   A
-constexpr int B_G = B_A + C * C * 4;            // f32  [C] G_t
-constexpr int B_EG = B_G + C * 4;               // f32  [C] 2^{G_t}
+constexpr int B_EG = B_VT + DH * SV * 2;        // f32  [C] 2^{G_t}
 constexpr int B_EH = B_EG + C * 4;              // f32  [C] 2^{G_C - G_t}
-constexpr int B_BETA = B_EH + C * 4;            // f32  [C]
-constexpr int BUF = B_BETA + C * 4;
-constexpr int OFF_T = 2 * BUF;                  // f32  [C][C]
-constexpr int OFF_TPH = OFF_T + C * C * 4;      // bf16 [C][SP]
-constexpr int OFF_TPL = OFF_TPH + C * SP * 2;
-constexpr int LDS_BYTES = OFF_TPL + C * SP * 2;
+constexpr int BUF = B_EH + C * 4;
+constexpr int OFF_ROWS = 2 * BUF;               // int64 [D] fused: checkpoint row table
+constexpr int LDS_BYTES = OFF_ROWS + D * 8;
 static_assert(BUF % 16 == 0 && LDS_BYTES <= 81920, "two blocks per CU");
 
 // One DPP move: lane l takes v from the lane CTRL selects within its row of 16 (0 where
@@ -87,6 +97,20 @@ __device__ inline float scan32(float x) {
   return x;
 }
 
+// Cumulative log2-decay of a chunk: lane t < 32 ends with G_t (lanes 32..63 hold sums
+// of zeros and are not used).
+__device__ inline float chunk_log2_decay(float graw, int lane) {
+  return scan32(lane < C ? fmaxf(graw, kGateFloor) * kLog2e : 0.f);
+}
+
+// Does head h of layer `layer` have an omitted row?  Every thread of the block must call
+// it (it is a block barrier).
+__device__ inline bool head_refreshed(const int32_t* inv_row, int64_t head_row, int tid) {
+  bool mine = false;
+  if (tid < D) mine = inv_row[head_row + tid] < 0;
+  return __syncthreads_or(mine);
+}
+
 // Blocks are dealt to the eight XCDs in turn (block b starts on XCD b mod 8).  Renumber
 // them so that each XCD takes a contiguous range of (request, head, half) items: the
 // blocks that read one key head (both halves of every v-head in its group) then sit on
@@ -96,27 +120,140 @@ __device__ inline int xcd_major(int b, int n_blocks) {
   return (b & 7) * (n_blocks >> 3) + (b >> 3);
 }
 
-// FUSED: the initial state comes from the packed checkpoint (kept rows from their
-// packed position, written back to the pool at once; omitted rows +0.0) and every row
-// of the layer is written, as the channel-wise kernel's fused variant does.
+// ---------------------------------------------------------------------------------------
+// -T' for chunk c of (request n, head h): wave w of block (n H + h) * per_head + j takes
+// chunk 4 j + w.  Heads with no omitted row are skipped.  The waves of a block share
+// nothing after the first barrier.
+__global__ __launch_bounds__(256) void gdn_factor_kernel(
+    int H, int Hqk, int layer, const int32_t* __restrict__ inv_row, const uint16_t* __restrict__ k,
+    const float* __restrict__ g, const float* __restrict__ beta, int W, int n_chunks,
+    uint4* __restrict__ ws) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[4 * F_WAVE];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int q = lane >> 4, r = lane & 15;
+  const int per_head = (n_chunks + 3) >> 2;
+  const int nh = blockIdx.x / per_head;
+  const int c = 4 * (blockIdx.x - nh * per_head) + w;
+  const int n = nh / H, h = nh - n * H;
+  if (!head_refreshed(inv_row, (int64_t(layer) * H + h) * D, tid)) return;
+  if (c >= n_chunks) return;   // a whole wave past the last chunk
+
+  float* sM = reinterpret_cast<float*>(smem + w * F_WAVE + F_M);
+  float* sG = reinterpret_cast<float*>(smem + w * F_WAVE + F_G);
+  float* sB = reinterpret_cast<float*>(smem + w * F_WAVE + F_B);
+
+  const int hk = h / (H / Hqk);
+  const __amdgpu_buffer_rsrc_t rk = rsrc(k + (int64_t(n) * Hqk + hk) * W * D, W * D * 2);
+  const __amdgpu_buffer_rsrc_t rg = rsrc(g + (int64_t(n) * H + h) * W, W * 4);
+  const __amdgpu_buffer_rsrc_t rb = rsrc(beta + (int64_t(n) * H + h) * W, W * 4);
+
+  // K K^T, three 16x16 tiles: lane (q, r) loads rows r and 16 + r at channels
+  // 32 kk + 8 q .. + 7, which are its A fragment for one tile and its B fragment for
+  // another (B[k][n] = K[n][k]).
+  bf16x8 f[2][4];
+#pragma unroll
+  for (int ti = 0; ti < 2; ++ti)
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+      f[ti][kk] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                                                 rk, ((16 * ti + r) * D + 32 * kk + 8 * q) * 2,
+                                                 c * C * D * 2, 0));
+  const float graw = lane < C ? ldf(rg, lane * 4, c * C * 4) : 0.f;
+  const float braw = lane < C ? ldf(rb, lane * 4, c * C * 4) : 0.f;
+  const float G = chunk_log2_decay(graw, lane);
+  if (lane < C) {
+    sG[lane] = G;
+    sB[lane] = braw;
+  }
+  f32x4 acc[3];
+#pragma unroll
+  for (int tile = 0; tile < 3; ++tile) {
+    const int ti = tile == 0 ? 0 : 1, si = tile == 2 ? 1 : 0;
+    acc[tile] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) acc[tile] = mma(f[ti][kk], f[si][kk], acc[tile]);
+  }
+  wave_lds_sync();
+  // A = Diag(beta) (strictly lower part of K K^T scaled by 2^{G_t - G_s})
+#pragma unroll
+  for (int tile = 0; tile < 3; ++tile) {
+    const int ti = tile == 0 ? 0 : 1, si = tile == 2 ? 1 : 0;
+    const int s = 16 * si + r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = 16 * ti + 4 * q + i;
+      sM[t * SA + s] = s < t ? sB[t] * acc[tile][i] * ex2(sG[t] - sG[s]) : 0.f;
+    }
+  }
+  wave_lds_sync();
+
+  // T = (I + A)^{-1}: diagonal 16x16 blocks by forward substitution, lane = column;
+  // row t of T replaces row t of A once every lane has read it (the wave runs in step)
+  if (lane < 32) {
+    const int base = 16 * (lane >> 4), s = lane & 15;
+    float x[16];
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      float a = (t == s) ? 1.f : 0.f;
+#pragma unroll
+      for (int rr = 0; rr < t; ++rr) a = fmaf(-sM[(base + t) * SA + base + rr], x[rr], a);
+      x[t] = a;
+      sM[(base + t) * SA + base + s] = a;
+    }
+  }
+  wave_lds_sync();
+
+  // T10 = -T11 (A10 T00) on fp32 MFMA, the product staying in registers between the
+  // steps; it then takes A10's place
+  {
+    f32x4 y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) y = mma32(sM[(16 + r) * SA + 4 * q + i], sM[(4 * q + i) * SA + r], y);
+    f32x4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) z = mma32(sM[(16 + r) * SA + 16 + 4 * q + i], y[i], z);
+    wave_lds_sync();   // every lane's reads of A10 are done
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sM[(16 + 4 * q + i) * SA + r] = -z[i];
+  }
+  wave_lds_sync();
+
+  // -T' = -T Diag(beta) in the U contraction's operand order, split hi/lo
+  uint4* out = ws + ((int64_t(n) * H + h) * n_chunks + c) * TP_VEC;
+#pragma unroll
+  for (int mu = 0; mu < 2; ++mu) {
+    const int t = 16 * mu + r;
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int s = e < 4 ? 4 * q + e : 16 + 4 * q + e - 4;
+      x[e] = s <= t ? -(sM[t * SA + s] * sB[s]) : 0.f;
+    }
+    bf16x8 hi, lo;
+    split8(x, hi, lo);
+    out[(2 * mu) * 64 + lane] = __builtin_bit_cast(uint4, hi);
+    out[(2 * mu + 1) * 64 + lane] = __builtin_bit_cast(uint4, lo);
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// The state recurrence over the window, -T' of every chunk read from the workspace.
+// FUSED: the initial state comes from the packed checkpoint (kept rows from their packed
+// position, written back to the pool at once; omitted rows +0.0) and every row of the
+// layer is written, as the channel-wise kernel's fused variant does.
 template <bool FUSED>
 __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     int H, int Hqk, int layer, int L, const int32_t* __restrict__ inv_row,
     float* __restrict__ states, int64_t n_pool, const int32_t* __restrict__ slot,
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, const float* __restrict__ g,
-    const float* __restrict__ beta, int W, int init_zero, dasc::CkptView ck) {
+    int W, int init_zero, dasc::CkptView ck, const uint4* __restrict__ ws, int n_chunks) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
-  float* sT = reinterpret_cast<float*>(smem + OFF_T);
-  __bf16* sTPH = reinterpret_cast<__bf16*>(smem + OFF_TPH);
-  __bf16* sTPL = reinterpret_cast<__bf16*>(smem + OFF_TPL);
   auto bK = [&](int b) { return reinterpret_cast<uint16_t*>(smem + b * BUF + B_K); };
   auto bKT = [&](int b) { return reinterpret_cast<uint16_t*>(smem + b * BUF + B_KT); };
   auto bVT = [&](int b) { return reinterpret_cast<uint16_t*>(smem + b * BUF + B_VT); };
-  auto bA = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_A); };
-  auto bG = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_G); };
   auto bEG = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_EG); };
   auto bEH = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_EH); };
-  auto bBeta = [&](int b) { return reinterpret_cast<float*>(smem + b * BUF + B_BETA); };
 
   const int item = xcd_major(blockIdx.x, gridDim.x);
   const int half = item & 1;
@@ -128,9 +265,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
   const int q = lane >> 4, r = lane & 15;
 
   const int64_t head_row = (int64_t(layer) * H + h) * D;
-  bool mine = false;
-  if (tid < D) mine = inv_row[head_row + tid] < 0;
-  const bool any_omitted = __syncthreads_or(mine);
+  const bool any_omitted = head_refreshed(inv_row, head_row, tid);
   if (!FUSED && !any_omitted) return;
   const int64_t sl = slot[n];
   if (sl < 0 || sl >= n_pool) return;
@@ -142,10 +277,8 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     if (cslot < 0 || cslot >= ck.n_slots) return;
   }
   // Fused: the head's checkpoint row table (float offsets, or dasc::kOmitted /
-  // dasc::kNoRow), in buffer 1's A tile, which the pipeline first writes two barriers
-  // after the initial state has been read.
-  int64_t* sOff = reinterpret_cast<int64_t*>(smem + BUF + B_A);
-  static_assert(D * 8 <= C * C * 4, "row table must fit in an A tile");
+  // dasc::kNoRow).
+  int64_t* sOff = reinterpret_cast<int64_t*>(smem + OFF_ROWS);
   if (FUSED) {
     if (tid < D) sOff[tid] = dasc::ckpt_row_offset(inv_row[head_row + tid], ck, cslot, D);
     __syncthreads();
@@ -182,215 +315,111 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
   const uint16_t* kp = k + (int64_t(n) * Hqk + hk) * W * D;
   const uint16_t* vp = v + (int64_t(n) * H + h) * W * D;
   const float* gp = g + (int64_t(n) * H + h) * W;
-  const float* bp = beta + (int64_t(n) * H + h) * W;
   const __amdgpu_buffer_rsrc_t rk = rsrc(kp, W * D * 2), rv = rsrc(vp, W * D * 2);
-  const __amdgpu_buffer_rsrc_t rg = rsrc(gp, W * 4), rb = rsrc(bp, W * 4);
+  const __amdgpu_buffer_rsrc_t rg = rsrc(gp, W * 4);
+  const uint4* tp = ws + (int64_t(n) * H + h) * n_chunks * TP_VEC;
 
-  // Waves 1-3 (192 threads, index st = tid - 64) load and stage a chunk:
-  //   keys row-major: 8-channel units u = st + 192 i (< 512): token u / 16, channels 8 (u % 16);
-  //   keys transposed: items p (< 256): channels 2 (p % 64), +1, tokens 8 (p / 64) .. +7;
-  //   values: items p (< 256): columns 64 half + 2 (p % 32), +1, tokens 4 (p / 32) .. +3;
-  //     item p = st for every wave and, on wave 3, also 192 + lane (wave 1 sums the gates);
-  //   gate and beta: token st % 32 (wave 1 sums them).
-  const int st = tid - 64;
-  uint4 kraw[3];
-  uint32_t kw[2][8], vw[2][4];
-  float graw = 0.f, braw = 0.f;
+  // Each thread loads and stages a chunk's
+  //   keys row-major: 8-channel units u = tid and 256 + tid: token u / 16, channels 8 (u % 16);
+  //   keys transposed: channels 2 (tid % 64), +1 at tokens 8 (tid / 64) .. +7;
+  //   values: columns 64 half + 2 (tid % 32), +1 at tokens 4 (tid / 32) .. +3;
+  // and lanes 0..31 of wave 0 its gates (summed there).
+  uint4 kraw[2];
+  uint32_t kw[8], vw[4];
+  float graw = 0.f;
   auto fetch = [&](int c0) {
 #pragma unroll
-    for (int i = 0; i < 3; ++i) {
-      const int u = st + 192 * i;
-      if (u < 512)
-        kraw[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                rk, ((u >> 4) * D + (u & 15) * 8) * 2, c0 * D * 2, 0));
-    }
-#pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int p = i == 0 ? st : (w == 3 ? 192 + lane : 256);
-      if (p < 256) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          kw[i][j] = __builtin_amdgcn_raw_buffer_load_b32(rk, ((8 * (p >> 6) + j) * D + 2 * (p & 63)) * 2,
-                                                          c0 * D * 2, 0);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          vw[i][j] = __builtin_amdgcn_raw_buffer_load_b32(
-              rv, ((4 * (p >> 5) + j) * D + DH * half + 2 * (p & 31)) * 2, c0 * D * 2, 0);
-      }
+      const int u = tid + 256 * i;
+      kraw[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                              rk, ((u >> 4) * D + (u & 15) * 8) * 2, c0 * D * 2, 0));
     }
-    graw = ldf(rg, (st & (C - 1)) * 4, c0 * 4);
-    braw = ldf(rb, (st & (C - 1)) * 4, c0 * 4);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      kw[j] = __builtin_amdgcn_raw_buffer_load_b32(rk, ((8 * (tid >> 6) + j) * D + 2 * (tid & 63)) * 2,
+                                                   c0 * D * 2, 0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      vw[j] = __builtin_amdgcn_raw_buffer_load_b32(
+          rv, ((4 * (tid >> 5) + j) * D + DH * half + 2 * (tid & 31)) * 2, c0 * D * 2, 0);
+    if (w == 0) graw = ldf(rg, (lane & (C - 1)) * 4, c0 * 4);
   };
   auto stage = [&](int b) {
     uint16_t* sK = bK(b);
     uint16_t* sKT = bKT(b);
     uint16_t* sVT = bVT(b);
 #pragma unroll
-    for (int i = 0; i < 3; ++i) {
-      const int u = st + 192 * i;
-      if (u < 512) *reinterpret_cast<uint4*>(sK + (u >> 4) * SK + (u & 15) * 8) = kraw[i];
-    }
-#pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int p = i == 0 ? st : (w == 3 ? 192 + lane : 256);
-      if (p < 256) {
-        uint32_t lo[4], hi[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          lo[j] = __builtin_amdgcn_perm(kw[i][2 * j + 1], kw[i][2 * j], 0x05040100u);
-          hi[j] = __builtin_amdgcn_perm(kw[i][2 * j + 1], kw[i][2 * j], 0x07060302u);
-        }
-        const int c2 = 2 * (p & 63), t8 = 8 * (p >> 6);
-        *reinterpret_cast<uint4*>(sKT + c2 * SV + t8) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-        *reinterpret_cast<uint4*>(sKT + (c2 + 1) * SV + t8) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-        const uint32_t vlo0 = __builtin_amdgcn_perm(vw[i][1], vw[i][0], 0x05040100u);
-        const uint32_t vlo1 = __builtin_amdgcn_perm(vw[i][3], vw[i][2], 0x05040100u);
-        const uint32_t vhi0 = __builtin_amdgcn_perm(vw[i][1], vw[i][0], 0x07060302u);
-        const uint32_t vhi1 = __builtin_amdgcn_perm(vw[i][3], vw[i][2], 0x07060302u);
-        const int v2 = 2 * (p & 31), t4 = 4 * (p >> 5);
-        *reinterpret_cast<uint2*>(sVT + v2 * SV + t4) = make_uint2(vlo0, vlo1);
-        *reinterpret_cast<uint2*>(sVT + (v2 + 1) * SV + t4) = make_uint2(vhi0, vhi1);
-      }
+      const int u = tid + 256 * i;
+      *reinterpret_cast<uint4*>(sK + (u >> 4) * SK + (u & 15) * 8) = kraw[i];
     }
-    if (w == 1) {   // inclusive running sum of the log2 gates over lanes 0..31
-      const float x = scan32(lane < C ? fmaxf(graw, kGateFloor) * kLog2e : 0.f);
+    {
+      uint32_t lo[4], hi[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        lo[j] = __builtin_amdgcn_perm(kw[2 * j + 1], kw[2 * j], 0x05040100u);
+        hi[j] = __builtin_amdgcn_perm(kw[2 * j + 1], kw[2 * j], 0x07060302u);
+      }
+      const int c2 = 2 * (tid & 63), t8 = 8 * (tid >> 6);
+      *reinterpret_cast<uint4*>(sKT + c2 * SV + t8) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      *reinterpret_cast<uint4*>(sKT + (c2 + 1) * SV + t8) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+      const uint32_t vlo0 = __builtin_amdgcn_perm(vw[1], vw[0], 0x05040100u);
+      const uint32_t vlo1 = __builtin_amdgcn_perm(vw[3], vw[2], 0x05040100u);
+      const uint32_t vhi0 = __builtin_amdgcn_perm(vw[1], vw[0], 0x07060302u);
+      const uint32_t vhi1 = __builtin_amdgcn_perm(vw[3], vw[2], 0x07060302u);
+      const int v2 = 2 * (tid & 31), t4 = 4 * (tid >> 5);
+      *reinterpret_cast<uint2*>(sVT + v2 * SV + t4) = make_uint2(vlo0, vlo1);
+      *reinterpret_cast<uint2*>(sVT + (v2 + 1) * SV + t4) = make_uint2(vhi0, vhi1);
+    }
+    if (w == 0) {
+      const float x = chunk_log2_decay(graw, lane);
       const float gc = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), C - 1));
       if (lane < C) {
-        bG(b)[lane] = x;
         bEG(b)[lane] = ex2(x);
         bEH(b)[lane] = ex2(gc - x);
-        bBeta(b)[lane] = braw;
       }
     }
   };
-  // A of the chunk in buffer b, strictly lower, tile (0,0), (1,0) or (1,1)
-  auto a_tile = [&](int b, int tile) {
-    const uint16_t* sK = bK(b);
-    const float* sG = bG(b);
-    const float* sBeta = bBeta(b);
-    float* sA = bA(b);
+  // -T' of a chunk, straight into the U phase's A operands (hi, lo per row tile)
+  uint4 tpr[4];
+  auto fetch_tp = [&](int ci) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) tpr[e] = tp[int64_t(ci) * TP_VEC + e * 64 + lane];
+  };
+
+  // prologue: chunk 0 staged, chunk 1 and the first factors in flight
+  fetch(0);
+  stage(0);
+  fetch(C);
+  fetch_tp(0);
+  __syncthreads();
+
+  for (int t0 = 0, b = 0, ci = 0; t0 < W; t0 += C, b ^= 1, ++ci) {
+    // ---- X = Diag(2^G) (K S') on this wave's columns ---------------------------------
+    f32x4 X[2] = {};
     {
-      const int ti = tile == 0 ? 0 : 1, si = tile == 2 ? 1 : 0;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      const __bf16* sK = reinterpret_cast<const __bf16*>(bK(b));
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 a8 = *reinterpret_cast<const bf16x8*>(sK + (16 * ti + r) * SK + 32 * kk + 8 * q);
-        const bf16x8 b8 = *reinterpret_cast<const bf16x8*>(sK + (16 * si + r) * SK + 32 * kk + 8 * q);
-        acc = mma(a8, b8, acc);
-      }
-      const int s = 16 * si + r;
+        bf16x8 sh, slo;
+        {
+          float x[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int t = 16 * ti + 4 * q + i;
-        sA[t * C + s] = s < t ? sBeta[t] * acc[i] * ex2(sG[t] - sG[s]) : 0.f;
-      }
-    }
-  };
-  // X = Diag(2^G) (K S') on this wave's columns
-  auto form_x = [&](int b, f32x4* X) {
-    const __bf16* sK = reinterpret_cast<const __bf16*>(bK(b));
-    X[0] = f32x4{0.f, 0.f, 0.f, 0.f};
-    X[1] = X[0];
+          for (int e = 0; e < 8; ++e) x[e] = S[2 * kk + (e >> 2)][e & 3];
+          split8(x, sh, slo);
+        }
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      bf16x8 sh, slo;
-      {
-        float x[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = S[2 * kk + (e >> 2)][e & 3];
-        split8(x, sh, slo);
-      }
-#pragma unroll
-      for (int mu = 0; mu < 2; ++mu) {
-        const bf16x8 kk8 = ld_op(sK + (16 * mu + r) * SK + 32 * kk + 4 * q);
-        X[mu] = mma(kk8, slo, X[mu]);
-        X[mu] = mma(kk8, sh, X[mu]);
-      }
-    }
-#pragma unroll
-    for (int mu = 0; mu < 2; ++mu) X[mu] *= *reinterpret_cast<const f32x4*>(bEG(b) + 16 * mu + 4 * q);
-  };
-
-  // prologue: chunk 0 staged and its A built; chunk 1 in flight
-  if (w > 0) fetch(0);
-  if (w > 0) stage(0);
-  __syncthreads();
-  if (w != 1) a_tile(0, w == 0 ? 0 : w - 1);
-  if (w > 0) fetch(C);
-  __syncthreads();
-
-  for (int t0 = 0, b = 0; t0 < W; t0 += C, b ^= 1) {
-    const bool more = t0 + C < W;
-    f32x4 X[2];
-    // ---- P1: T = (I + A)^{-1} diagonal blocks (wave 0) | X and the next chunk's staging
-    if (w == 0) {
-      if (lane < 32) {
-        const float* sA = bA(b);
-        const int base = 16 * (lane >> 4), s = lane & 15;
-        float x[16];
-#pragma unroll
-        for (int t = 0; t < 16; ++t) {
-          float a = (t == s) ? 1.f : 0.f;
-#pragma unroll
-          for (int rr = 0; rr < t; ++rr) a = fmaf(-sA[(base + t) * C + base + rr], x[rr], a);
-          x[t] = a;
-          sT[(base + t) * C + base + s] = a;
+        for (int mu = 0; mu < 2; ++mu) {
+          const bf16x8 kk8 = ld_op(sK + (16 * mu + r) * SK + 32 * kk + 4 * q);
+          X[mu] = mma(kk8, slo, X[mu]);
+          X[mu] = mma(kk8, sh, X[mu]);
         }
       }
-    } else {
-      form_x(b, X);
-      if (more) stage(b ^ 1);
+#pragma unroll
+      for (int mu = 0; mu < 2; ++mu) X[mu] *= *reinterpret_cast<const f32x4*>(bEG(b) + 16 * mu + 4 * q);
     }
-    __syncthreads();
 
-    // ---- P2: X (wave 0) | -T' = -T Diag(beta) split (negated so that U takes X - V, one
-    //          dot2 per value), T10 = -T11 (A10 T00) on wave 1 |
-    //          the next chunk's A tiles (waves 2-3) | loads of the chunk after next
-    {
-      const float* sA = bA(b);
-      const float* sBeta = bBeta(b);
-      if (w == 0) {
-        form_x(b, X);
-        if (more) a_tile(b ^ 1, 0);   // the next chunk's A: tile (0,0) here, the others on waves 2-3
-      } else if (w == 1) {
-        f32x4 y = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          y = mma32(sA[(16 + r) * C + 4 * q + i], sT[(4 * q + i) * C + r], y);
-        f32x4 z = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) z = mma32(sT[(16 + r) * C + 16 + 4 * q + i], y[i], z);
-        const float br = sBeta[r];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int t = 16 + 4 * q + i;
-          __bf16 a, bb;
-          split(z[i] * br, a, bb);   // -T'10
-          sTPH[t * SP + r] = a;
-          sTPL[t * SP + r] = bb;
-        }
-      }
-      if (w >= 1) {
-        // 768 entries outside block (1,0): rows 0..15 whole, rows 16..31 columns 16..31,
-        // over waves 1-3 (wave 1 after its T10)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int e = st + 192 * u;
-          const int t = e < 512 ? e >> 5 : 16 + ((e - 512) >> 4);
-          const int s = e < 512 ? e & 31 : 16 + ((e - 512) & 15);
-          const float val = s <= t ? sT[t * C + s] * sBeta[s] : 0.f;
-          __bf16 a, bb;
-          split(-val, a, bb);
-          sTPH[t * SP + s] = a;
-          sTPL[t * SP + s] = bb;
-        }
-        if (w >= 2 && more) a_tile(b ^ 1, w - 1);
-        if (t0 + 2 * C < W) fetch(t0 + 2 * C);
-      }
-    }
-    __syncthreads();
-
-    // ---- P3: U = (-T')(X - V), Diag(2^{G_C - G}) U, S' <- 2^{G_C} S' + K^T U ----------
+    // ---- U = (-T')(X - V), Diag(2^{G_C - G}) U, S' <- 2^{G_C} S' + K^T U ----------------
     {
       const uint16_t* sVT = bVT(b);
       const float* sEH = bEH(b);
@@ -407,13 +436,14 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       split8(x, yh, yl);
 #pragma unroll
       for (int mu = 0; mu < 2; ++mu) {
-        const int o = (16 * mu + r) * SP + 4 * q;
-        const bf16x8 ah = ld_op(sTPH + o), al = ld_op(sTPL + o);
+        const bf16x8 ah = __builtin_bit_cast(bf16x8, tpr[2 * mu]);
+        const bf16x8 al = __builtin_bit_cast(bf16x8, tpr[2 * mu + 1]);
         f32x4 c = mma(al, yh, f32x4{0.f, 0.f, 0.f, 0.f});
         c = mma(ah, yl, c);
         U[mu] = mma(ah, yh, c);
         U[mu] *= *reinterpret_cast<const f32x4*>(sEH + 16 * mu + 4 * q);
       }
+      if (t0 + C < W) fetch_tp(ci + 1);
       bf16x8 uh, ul;
       {
         float xu[8];
@@ -430,6 +460,12 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
         S[mt] = mma(kt8, uh, S[mt]);
       }
     }
+
+    // ---- the next chunk into the other buffer; the one after that into registers --------
+    if (t0 + C < W) {
+      stage(b ^ 1);
+      if (t0 + 2 * C < W) fetch(t0 + 2 * C);
+    }
     __syncthreads();
   }
 
@@ -442,18 +478,38 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     }
 }
 
+inline int gdn_chunks(int W) { return (W + C - 1) / C; }
+
+void launch_factors(int n_req, int H, int Hqk, int layer, const int32_t* inv_row, const uint16_t* k,
+                    const float* g, const float* beta, int W, void* ws, hipStream_t st) {
+  const int n_chunks = gdn_chunks(W);
+  const dim3 grid(unsigned(n_req) * unsigned(H) * unsigned((n_chunks + 3) / 4)), block(256);
+  hipLaunchKernelGGL(gdn_factor_kernel, grid, block, 0, st, H, Hqk, layer, inv_row, k, g, beta, W,
+                     n_chunks, static_cast<uint4*>(ws));
+}
+
 }  // namespace
 
 namespace dasc {
 
+size_t gdn_factor_workspace_bytes(int n_req, int H, int W) {
+  return size_t(n_req) * size_t(H) * size_t(gdn_chunks(W)) * size_t(kGdnFactorBytesPerChunk);
+}
+
+int64_t gdn_factor_blocks(int n_req, int H, int W) {
+  return int64_t(n_req) * H * ((gdn_chunks(W) + 3) / 4);
+}
+
 void launch_refresh_wy_gdn(int n_req, int H, int Hqk, int layer, int L, const int32_t* inv_row,
                            float* states, int64_t n_pool, const int32_t* slot, const uint16_t* k,
                            const uint16_t* v, const float* g, const float* beta, int W,
-                           int init_zero, hipStream_t st) {
+                           int init_zero, void* ws, hipStream_t st) {
+  launch_factors(n_req, H, Hqk, layer, inv_row, k, g, beta, W, ws, st);
   const dim3 grid(unsigned(n_req) * unsigned(H) * 2u), block(256);
   const CkptView none{nullptr, 1, 1, 0, nullptr};
   hipLaunchKernelGGL(refresh_wy_gdn_kernel<false>, grid, block, 0, st, H, Hqk, layer, L, inv_row,
-                     states, n_pool, slot, k, v, g, beta, W, init_zero, none);
+                     states, n_pool, slot, k, v, g, W, init_zero, none,
+                     static_cast<const uint4*>(ws), gdn_chunks(W));
 }
 
 void launch_restore_refresh_wy_gdn(int n_req, int H, int Hqk, int layer, int L, const float* ckpt,
@@ -461,11 +517,14 @@ void launch_restore_refresh_wy_gdn(int n_req, int H, int Hqk, int layer, int L, 
                                    int64_t slice_rows, int64_t n_rows, const int32_t* inv_row,
                                    float* states, int64_t n_pool, const int32_t* slot,
                                    const uint16_t* k, const uint16_t* v, const float* g,
-                                   const float* beta, int W, int init_zero, hipStream_t st) {
+                                   const float* beta, int W, int init_zero, void* ws,
+                                   hipStream_t st) {
+  launch_factors(n_req, H, Hqk, layer, inv_row, k, g, beta, W, ws, st);
   const dim3 grid(unsigned(n_req) * unsigned(H) * 2u), block(256);
   const CkptView ck{ckpt, n_ckpt_slots, slice_rows, n_rows, ck_slot};
   hipLaunchKernelGGL(refresh_wy_gdn_kernel<true>, grid, block, 0, st, H, Hqk, layer, L, inv_row,
-                     states, n_pool, slot, k, v, g, beta, W, init_zero, ck);
+                     states, n_pool, slot, k, v, g, W, init_zero, ck,
+                     static_cast<const uint4*>(ws), gdn_chunks(W));
 }
 
 }  // namespace dasc

@@ -279,6 +279,22 @@ def dasc_refresh_workspace_bytes(shape: Shape, n_req: int, W: int) -> int:
     return out.value
 
 
+def _workspace(shape: Shape, n_req: int, W: int, workspace, device, stream):
+    """(pointer, bytes) of the refresh workspace: the caller's uint8 device tensor, or one
+    drawn from torch's allocator when none is given and the call needs it.  A drawn one is
+    tied to the launch stream, so torch does not hand it out again before the launch ends."""
+    import torch
+
+    if workspace is None:
+        need = dasc_refresh_workspace_bytes(shape, n_req, W)
+        if need == 0:
+            return None, 0
+        workspace = torch.empty(need, dtype=torch.uint8, device=device)
+        if stream is not None:
+            workspace.record_stream(stream)
+    return _dev(workspace, torch.uint8, "workspace"), workspace.numel()
+
+
 def dasc_refresh(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta, W: int,
                  init_mode: str = "restored", workspace=None, stream=None) -> None:
     """Refresh one layer's omitted units for every request in `slot`.
@@ -295,9 +311,7 @@ def dasc_refresh(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta,
     _need(v, n_req * H * W * dv, "v")
     _need(g, n_req * H * W * (dk if shape.arch == "kda" else 1), "g")
     _need(beta, n_req * H * W, "beta")
-    ws_ptr, ws_bytes = None, 0
-    if workspace is not None:
-        ws_ptr, ws_bytes = _dev(workspace, torch.uint8, "workspace"), workspace.numel()
+    ws_ptr, ws_bytes = _workspace(shape, n_req, W, workspace, states.device, stream)
     _check(LIB.dasc_refresh(
         C.byref(shape.c()), layer, _dev(inv_row, torch.int32, "inv_row"),
         _dev(states, torch.float32, "states"), states.shape[0], _dev(slot, torch.int32, "slot"),
@@ -327,9 +341,7 @@ def dasc_restore_refresh(shape: Shape, layer: int, ckpt, src_slot, inv_row, stat
     _need(v, n_req * H * W * dv, "v")
     _need(g, n_req * H * W * (dk if shape.arch == "kda" else 1), "g")
     _need(beta, n_req * H * W, "beta")
-    ws_ptr, ws_bytes = None, 0
-    if workspace is not None:
-        ws_ptr, ws_bytes = _dev(workspace, torch.uint8, "workspace"), workspace.numel()
+    ws_ptr, ws_bytes = _workspace(shape, n_req, W, workspace, states.device, stream)
     _check(LIB.dasc_restore_refresh(
         C.byref(shape.c()), layer, _dev(ckpt, torch.float32, "ckpt"), n_slots,
         _dev(src_slot, torch.int32, "src_slot"), n_ranks, slice_rows, n_rows,

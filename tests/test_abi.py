@@ -197,6 +197,29 @@ def test_refresh_argument_errors():
     need = C.c_size_t(99)
     assert LIB.dasc_refresh_workspace_bytes(C.byref(kda()), 1, 0, C.byref(need)) == E.DASC_E_INVAL
     assert LIB.dasc_refresh_workspace_bytes(C.byref(kda()), 2, 64, C.byref(need)) == E.DASC_OK
+    assert need.value == 0
+
+
+def test_gdn_refresh_workspace():
+    # GDN heads at dk = dv = 128 keep one 4 KiB factor per (request, head, 32-token chunk)
+    E = _lib
+    gdn = Shape(_lib.DASC_ARCH_GDN, 2, 32, 16, 128, 128)
+    need = C.c_size_t(0)
+    for n_req, W in ((8, 1024), (1, 1), (3, 33), (2, 2048)):
+        assert LIB.dasc_refresh_workspace_bytes(C.byref(gdn), n_req, W, C.byref(need)) == E.DASC_OK
+        assert need.value == n_req * 32 * (-(-W // 32)) * 4096
+    # other shapes need none
+    for sh in (Shape(_lib.DASC_ARCH_GDN, 1, 4, 2, 64, 64), kda(dk=128, dv=128)):
+        assert LIB.dasc_refresh_workspace_bytes(C.byref(sh), 4, 256, C.byref(need)) == E.DASC_OK
+        assert need.value == 0
+    W, n_req = 64, 2
+    full = n_req * 32 * 2 * 4096
+    assert refresh(gdn, W=W, n_req=n_req) == E.DASC_E_WORKSPACE                       # none
+    assert refresh(gdn, W=W, n_req=n_req, ws=FAKE, ws_bytes=full - 1) == E.DASC_E_WORKSPACE
+    assert refresh(gdn, W=W, n_req=n_req, ws=None, ws_bytes=full) == E.DASC_E_WORKSPACE
+    assert refresh(gdn, W=W, n_req=n_req, ws=FAKE_ODD, ws_bytes=full) == E.DASC_E_INVAL
+    assert restore_refresh(gdn, W=W, n_req=n_req) == E.DASC_E_WORKSPACE
+    assert restore_refresh(gdn, W=W, n_req=n_req, ws=FAKE_ODD, ws_bytes=full) == E.DASC_E_INVAL
 
 
 def test_plan_argument_errors():

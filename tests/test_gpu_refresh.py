@@ -177,7 +177,8 @@ def _inputs_128(arch, n_req, H, Hqk, W, seed, g_lo=None):
 
 @pytest.mark.parametrize("arch,W,g_lo", [
     ("kda", 1, None), ("kda", 31, None), ("kda", 33, None), ("kda", 100, None),
-    ("kda", 64, -30.0), ("gdn", 47, None), ("gdn", 96, -30.0),
+    ("kda", 64, -30.0), ("gdn", 1, None), ("gdn", 31, None), ("gdn", 33, None),
+    ("gdn", 47, None), ("gdn", 96, -30.0),
 ])
 def test_chunked_kernel_ragged_and_strong_decay(arch, W, g_lo):
     # dk = dv = 128 takes the chunked MFMA kernel; ragged last chunks and very strong
@@ -240,3 +241,36 @@ def test_gdn_scalar_gate_kernel_matches_channel_kernel(monkeypatch):
     scale = np.abs(b[:, layer][:, om]).max()
     announce(f"gdn scalar-gate vs channel kernel max diff / max {diff / scale:.2e}")
     assert diff <= 1e-4 * scale
+
+
+def test_gdn_workspace_reuse():
+    # the per-chunk factors live in a caller-owned workspace; one buffer reused by calls
+    # with different windows (the larger first, then a smaller one, which reads only
+    # what it wrote) gives the bits of a freshly drawn one
+    import torch
+
+    L, H, Hqk, n_req = 1, 4, 2, 3
+    sh = D.Shape("gdn", L, H, Hqk, 128, 128)
+    rng = np.random.default_rng(11)
+    g_static = D.dasc_static_log_decay(rng.uniform(math.log(1e-4), 0, size=(L, H)))
+    g_static[0, 0] = math.log(1e-3) / 2.0
+    g_static[0, 3] = math.log(1e-3) / 2.0
+    inv = D.dasc_plan(sh, g_static, "threshold", 0, 64)["inv_row"]
+    pool = (0.05 * rng.standard_normal((3, L, H, 128, 128))).astype(np.float32)
+    pool.reshape(3, -1, 128)[:, inv < 0] = 0.0
+    ws = torch.full((D.dasc_refresh_workspace_bytes(sh, n_req, 96),), 0x7F, dtype=torch.uint8,
+                    device="cuda")
+    for W in (96, 40):
+        inp = _inputs_128("gdn", n_req, H, Hqk, W, seed=W)
+        args = (dev_i32(inv), None, dev_i32([2, 0, 1]), dev_bf16(inp["k"]), dev_bf16(inp["v"]),
+                dev(inp["g"]), dev(inp["beta"]), W)
+        outs = []
+        for workspace in (ws, None):
+            states = dev(pool)
+            announce(f"gdn workspace reuse W={W} explicit={workspace is not None}")
+            D.dasc_refresh(sh, 0, args[0], states, *args[2:], workspace=workspace)
+            torch.cuda.synchronize()
+            outs.append(states.cpu().numpy())
+        assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+        check(sh, pool, outs[0], 0, inv, inp, [(n, h) for n in range(n_req) for h in range(H)],
+              slots=[2, 0, 1])
