@@ -240,11 +240,37 @@ def bench_headline(torch, args):
     heads_refreshed = int(omitted.any(axis=1).sum())
     bytes_pack = 2 * R * dv * 4 * n_ckpt
     bytes_restore = (R + rows) * dv * 4 * n_ckpt
-    # refresh reads k, v, g, beta and the restored state of every refreshed head, and
-    # writes the omitted rows
-    per_head = (2 * W * sh.dk + 2 * W * dv + 4 * W * sh.dk + 4 * W + 4 * sh.dk * dv)
-    bytes_refresh = n_req * (heads_refreshed * per_head + int(omitted.sum()) * dv * 4)
+
+    def refresh_bytes(w):
+        # refresh reads k, v, g, beta and the restored state of every refreshed head, and
+        # writes the omitted rows
+        per_head = (2 * w * sh.dk + 2 * w * dv + 4 * w * sh.dk + 4 * w + 4 * sh.dk * dv)
+        return per_head, n_req * (heads_refreshed * per_head + int(omitted.sum()) * dv * 4)
+
+    per_head, bytes_refresh = refresh_bytes(W)
     flops_refresh = WY_FLOP_PER_HEAD_TOKEN * W * n_req * heads_refreshed
+
+    # the serving shape's other replay windows (refresh alone, same requests and state)
+    by_window = {}
+    for w2 in wl.windows:
+        if w2 == W:
+            continue
+        inp2 = refresh_inputs(wl, w2, log_lambda(wl)[0], salt=w2)
+        k2, v2 = _bf16(torch, inp2["k"]), _bf16(torch, inp2["v"])
+        g2, b2 = torch.from_numpy(inp2["g"]).cuda(), torch.from_numpy(inp2["beta"]).cuda()
+        name = f"refresh_W{w2}"
+        run2 = lambda: D.dasc_refresh(sh, 0, inv_row, active, req, k2, v2, g2, b2, w2)  # noqa: E731
+        for _ in range(args.warmup):
+            run2()
+        torch.cuda.synchronize()
+        for _ in range(args.steps):
+            timer.run(name, run2)
+        torch.cuda.synchronize()
+        ms2 = timer.mean_ms(name)
+        by_window[str(w2)] = {"ms": ms2, "tokens_per_s": n_req * w2 / (ms2 / 1e3),
+                              "GBps": refresh_bytes(w2)[1] / ms2 / 1e6,
+                              "hbm_frac": refresh_bytes(w2)[1] / ms2 / 1e6 / HBM_PEAK_GBPS}
+        del k2, v2, g2, b2
 
     t = {n: timer.mean_ms(n) for n in ("pack", "restore", "refresh", "restore_req", "refresh_req",
                                        "restore_refresh")}
@@ -265,6 +291,7 @@ def bench_headline(torch, args):
             "ms": t["restore_refresh"], "unfused_ms": t["restore_req"] + t["refresh_req"],
             "requests": n_req, "GBps": bytes_fused / t["restore_refresh"] / 1e6,
             "bytes": bytes_fused},
+        "refresh_by_window": by_window,
     }
     achieved = bytes_refresh / t["refresh"] / 1e6          # GB/s
     traffic = measured_traffic("kimi_headline/refresh")
