@@ -252,8 +252,9 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     __syncthreads();
 
     // ---- A = Diag(beta) (strictly lower part of R Q^T), three 16x16 tiles -----------
-    // fp32 MFMA (16x16x4): lane (q, r) feeds channel c = 16j + 4q + i to step (j, i), so
-    // the factors need no bf16 splitting.
+    // bf16 MFMA (16x16x32) on hi/lo split factors, like the state products: lane (q, r)
+    // feeds channels 32 kk + 8 q + e of its row to step kk (three MFMAs a step where fp32
+    // MFMA would take eight, at a sixteenth of the bf16 rate).
     if (w < 3) {
       const int ti = w == 0 ? 0 : 1, si = w == 2 ? 1 : 0;
       const int rf = w == 0 ? 8 : (w == 1 ? 15 : 24);   // reference token of the tile
@@ -261,25 +262,35 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
       // fully unrolled the reads and exponentials overlap best; the fused variant keeps
       // two steps, where the checkpoint row table already presses on registers
-      constexpr int kAUnroll = FUSED ? 2 : 8;
+      constexpr int kAUnroll = FUSED ? 2 : 4;
 #pragma unroll kAUnroll
-      for (int j = 0; j < 8; ++j) {
-        const int c0 = 16 * j + 4 * q;
-        const f32x4 gt = *reinterpret_cast<const f32x4*>(sG + tr * SG + c0);
-        const f32x4 gs = *reinterpret_cast<const f32x4*>(sG + sr * SG + c0);
-        const f32x4 gf = *reinterpret_cast<const f32x4*>(sG + rf * SG + c0);
-        const uint2 kt = *reinterpret_cast<const uint2*>(sK + tr * SK + c0);
-        const uint2 ks = *reinterpret_cast<const uint2*>(sK + sr * SK + c0);
-        const uint32_t ktw[2] = {kt.x, kt.y}, ksw[2] = {ks.x, ks.y};
+      for (int kk = 0; kk < 4; ++kk) {
+        const int c0 = 32 * kk + 8 * q;
+        float fa[8], fb[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float kte = __uint_as_float((i & 1) ? (ktw[i >> 1] & 0xFFFF0000u) : (ktw[i >> 1] << 16));
-          const float kse = __uint_as_float((i & 1) ? (ksw[i >> 1] & 0xFFFF0000u) : (ksw[i >> 1] << 16));
-          if (i & 1)
-            acc2 = mma32(kte * ex2(gt[i] - gf[i]), kse * ex2(gf[i] - gs[i]), acc2);
-          else
-            acc = mma32(kte * ex2(gt[i] - gf[i]), kse * ex2(gf[i] - gs[i]), acc);
+        for (int h2 = 0; h2 < 2; ++h2) {
+          const f32x4 gt = *reinterpret_cast<const f32x4*>(sG + tr * SG + c0 + 4 * h2);
+          const f32x4 gs = *reinterpret_cast<const f32x4*>(sG + sr * SG + c0 + 4 * h2);
+          const f32x4 gf = *reinterpret_cast<const f32x4*>(sG + rf * SG + c0 + 4 * h2);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            fa[4 * h2 + i] = ex2(gt[i] - gf[i]);
+            fb[4 * h2 + i] = ex2(gf[i] - gs[i]);
+          }
         }
+        const uint4 kt = *reinterpret_cast<const uint4*>(sK + tr * SK + c0);
+        const uint4 ks = *reinterpret_cast<const uint4*>(sK + sr * SK + c0);
+        const uint32_t ktw[4] = {kt.x, kt.y, kt.z, kt.w}, ksw[4] = {ks.x, ks.y, ks.z, ks.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          fa[e] *= __uint_as_float((e & 1) ? (ktw[e >> 1] & 0xFFFF0000u) : (ktw[e >> 1] << 16));
+          fb[e] *= __uint_as_float((e & 1) ? (ksw[e >> 1] & 0xFFFF0000u) : (ksw[e >> 1] << 16));
+        }
+        bf16x8 ah, al, bh, bl;
+        split8(fa, ah, al);
+        split8(fb, bh, bl);
+        if (kk & 1) acc2 = mma3(ah, al, bh, bl, acc2);
+        else acc = mma3(ah, al, bh, bl, acc);
       }
       acc += acc2;
 #pragma unroll
