@@ -49,7 +49,8 @@ __device__ inline void split(float x, __bf16& hi, __bf16& lo) {
 }
 
 // Eight values split at once: hi = bf16(x) two values per packed conversion, and the
-// remainder x - hi (exact in fp32) by one dot2 per value, so 2 VALU per value.
+// remainder x - hi (exact in fp32) by one dot2 per value: 2 VALU per value when x dies
+// here, 3 when x lives on (the accumulating dot then needs a copy of it first).
 __device__ inline void split8(const float* x, bf16x8& hi, bf16x8& lo) {
   uint32_t h[4], l[4];
 #pragma unroll
