@@ -178,7 +178,8 @@ def _inputs_128(arch, n_req, H, Hqk, W, seed, g_lo=None):
 @pytest.mark.parametrize("arch,W,g_lo", [
     ("kda", 1, None), ("kda", 31, None), ("kda", 33, None), ("kda", 100, None),
     ("kda", 64, -30.0), ("gdn", 1, None), ("gdn", 31, None), ("gdn", 33, None),
-    ("gdn", 47, None), ("gdn", 96, -30.0),
+    ("gdn", 47, None), ("gdn", 63, None), ("gdn", 65, None), ("gdn", 96, -30.0),
+    ("gdn", 129, None), ("gdn", 200, -30.0),
 ])
 def test_chunked_kernel_ragged_and_strong_decay(arch, W, g_lo):
     # dk = dv = 128 takes the chunked MFMA kernel; ragged last chunks and very strong
@@ -258,9 +259,9 @@ def test_gdn_workspace_reuse():
     inv = D.dasc_plan(sh, g_static, "threshold", 0, 64)["inv_row"]
     pool = (0.05 * rng.standard_normal((3, L, H, 128, 128))).astype(np.float32)
     pool.reshape(3, -1, 128)[:, inv < 0] = 0.0
-    ws = torch.full((D.dasc_refresh_workspace_bytes(sh, n_req, 96),), 0x7F, dtype=torch.uint8,
+    ws = torch.full((D.dasc_refresh_workspace_bytes(sh, n_req, 160),), 0x7F, dtype=torch.uint8,
                     device="cuda")
-    for W in (96, 40):
+    for W in (160, 40):
         inp = _inputs_128("gdn", n_req, H, Hqk, W, seed=W)
         args = (dev_i32(inv), None, dev_i32([2, 0, 1]), dev_bf16(inp["k"]), dev_bf16(inp["v"]),
                 dev(inp["g"]), dev(inp["beta"]), W)
