@@ -49,6 +49,9 @@ def parse():
                     choices=["kimi_headline", "kimi_model", "qwen_gdn"])
     ap.add_argument("--W", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-windows", action="store_true",
+                    help="time the refresh at the headline window only (counter runs average "
+                         "every dispatch of a kernel, so the other windows would mix in)")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
     return ap.parse_args()
@@ -253,7 +256,7 @@ def bench_headline(torch, args):
     # the serving shape's other replay windows (refresh alone, same requests and state)
     by_window = {}
     for w2 in wl.windows:
-        if w2 == W:
+        if w2 == W or args.no_other_windows:
             continue
         inp2 = refresh_inputs(wl, w2, log_lambda(wl)[0], salt=w2)
         k2, v2 = _bf16(torch, inp2["k"]), _bf16(torch, inp2["v"])
