@@ -58,12 +58,15 @@ def parse():
 
 
 def kernel_source_hash() -> str:
+    """Digest of everything that decides the device code: the kernel sources and headers,
+    and the build script with its compiler flags."""
     h = hashlib.sha256()
     for f in ("pack_restore.hip", "quant.hip", "refresh.hip", "refresh_wy.hip", "refresh_wy_gdn.hip",
-              "ckpt_layout.h",
-              "refresh_kernels.h", "launch_common.h"):
+              "ckpt_layout.h", "refresh_kernels.h", "launch_common.h", "wy_ops.h"):
         with open(os.path.join(ROOT, "paper_2608_30386_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
+    with open(os.path.join(ROOT, "paper_2608_30386_amd", "build.py"), "rb") as fh:
+        h.update(fh.read())
     return h.hexdigest()[:16]
 
 

@@ -3,7 +3,10 @@
     python paper_2608_30386_amd/build.py
 
 HIP sources are compiled by hipcc for gfx950 only; packed-FP32 instructions are
-disabled for all device code.  The planner is plain host C++ compiled by g++
+disabled for all device code, and so is the two-address bf16 dot product
+(v_dot2c_f32_bf16): the compiler then emits its three-address form (v_dot2_f32_bf16),
+whose result register differs from the accumulator, so splitting a value that stays
+live costs no copy.  The two forms give the same bits.  The planner is plain host C++ compiled by g++
 without fast-math or FP contraction, so its binary64 results are reproducible.
 """
 
@@ -36,6 +39,7 @@ def _hipcc() -> str:
 HIP_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Xclang", "-target-feature", "-Xclang", "-dot13-insts",
     "-Wall", "-Wno-unused-function",
 ]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-fast-math", "-Wall"]
