@@ -43,8 +43,11 @@ METRIC = "pack/restore GB/s + suffix-refresh tokens/s (KDA 32h x 128x128, W=1024
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    # From idle, the clock takes about 25 back-to-back steps to settle under this load: the
+    # refresh launch time climbs from 295 to 350 us and comes back to 300 us over the
+    # first 23 launches of a run, then stays at 280-300 us.
+    ap.add_argument("--warmup", type=int, default=25)
     ap.add_argument("--workload", default="kimi_headline",
                     choices=["kimi_headline", "kimi_model", "qwen_gdn"])
     ap.add_argument("--W", type=int, default=1024)
