@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 
 import paper_2608_30386_amd as D
+from paper_2608_30386_amd._lib import DASC_MAX_WINDOW
 from oracle import pack as OK
 from oracle import recurrence as OR
 from tests.gpu_util import announce, dev, dev_bf16, dev_i32, host_words, plans, shape_of
@@ -275,3 +276,49 @@ def test_gdn_workspace_reuse():
         assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
         check(sh, pool, outs[0], 0, inv, inp, [(n, h) for n in range(n_req) for h in range(H)],
               slots=[2, 0, 1])
+
+
+@pytest.mark.parametrize("arch", ["kda", "gdn"])
+def test_maximum_window(arch):
+    # W = DASC_MAX_WINDOW (2^21 tokens): every token but the last 1024 is an identity step
+    # (k = v = 0, g = 0, beta = 0: no decay, no update, exactly), so the result is the
+    # oracle's replay of those 1024 tokens from the restored state.  The kernels still walk
+    # the whole window: 65,536 chunks, input offsets up to 2^30 bytes, a 512 MiB GDN
+    # factor workspace.  GDN: two v-heads on one key head.
+    import torch
+
+    W, tail = DASC_MAX_WINDOW, 1024
+    L, H, n_req = 1, 2, 1
+    Hqk = 2 if arch == "kda" else 1
+    sh = D.Shape(arch, L, H, Hqk, 128, 128)
+    rng = np.random.default_rng(21)
+    unit_shape = (L, H, 128) if arch == "kda" else (L, H)
+    g_static = D.dasc_static_log_decay(rng.uniform(math.log(1e-4), 0, size=unit_shape))
+    g_static[0, 0] = math.log(1e-3) / 2.0             # head 0 (GDN) / row 0 (KDA) omitted
+    if arch == "gdn":
+        g_static[0, 1] = math.log(1e-3) / 1000.0      # head 1 kept
+    inv = D.dasc_plan(sh, g_static, "threshold", 0, 64)["inv_row"]
+    pool = (0.05 * rng.standard_normal((1, L, H, 128, 128))).astype(np.float32)
+    pool.reshape(1, -1, 128)[:, inv < 0] = 0.0
+    inp = _inputs_128(arch, n_req, H, Hqk, tail, seed=W)
+
+    def whole(x, bits=False):
+        shape = list(x.shape)
+        shape[2] = W
+        t = torch.zeros(shape, dtype=torch.bfloat16 if bits else torch.float32, device="cuda")
+        t[:, :, W - tail:] = dev_bf16(x) if bits else dev(x)
+        return t
+
+    k, v = whole(inp["k"], bits=True), whole(inp["v"], bits=True)
+    g, beta = whole(inp["g"]), whole(inp["beta"])
+    states = dev(pool)
+    announce(f"refresh {sh} n_req=1 W={W} (identity steps but the last {tail})")
+    D.dasc_refresh(sh, 0, dev_i32(inv), states, dev_i32([0]), k, v, g, beta, W)
+    torch.cuda.synchronize()
+    got = states.cpu().numpy()
+    del k, v, g, beta
+    om = (inv < 0).reshape(H, 128)
+    pairs = [(0, h) for h in range(H) if om[h].any()]
+    assert pairs
+    err = check(sh, pool, got, 0, inv, inp, pairs)
+    announce(f"maximum window {arch}: max rel err {err:.2e}")
