@@ -57,6 +57,8 @@ def parse():
                          "every dispatch of a kernel, so the other windows would mix in)")
     ap.add_argument("--copy-calib", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
+    ap.add_argument("--copy-bw", action="store_true",
+                    help="time only torch's device copy of 4 GiB (the box's plain-copy rate)")
     return ap.parse_args()
 
 
@@ -123,6 +125,26 @@ def copy_calibration(torch):
     print(json.dumps({"copy_calibration_bytes": n * 4, "launches": 3}))
 
 
+def copy_bandwidth(torch, args):
+    """torch's device-to-device copy of 4 GiB of fp32: the plain-copy rate of this machine, the
+    secondary reference for the pack and restore rates (bytes read + written per second)."""
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(args.warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    print(json.dumps({"copy_bytes": 2 * n * 4, "ms": ms, "GBps": 2 * n * 4 / ms / 1e6,
+                      "steps": args.steps, "warmup": args.warmup}))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -136,6 +158,9 @@ def main():
         sys.exit(2)
     if args.copy_calib:
         copy_calibration(torch)
+        return
+    if args.copy_bw:
+        copy_bandwidth(torch, args)
         return
     if args.workload == "kimi_headline":
         out = bench_headline(torch, args)
