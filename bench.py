@@ -126,7 +126,7 @@ def copy_calibration(torch):
 
 
 def copy_bandwidth(torch, args):
-    """torch's device-to-device copy of 4 GiB of fp32: the plain-copy rate of this machine, the
+    """torch's device-to-device copy of 4 GiB of fp32: the plain-copy rate of the GPU, the
     secondary reference for the pack and restore rates (bytes read + written per second)."""
     n = 1 << 30
     src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -148,7 +148,7 @@ def copy_bandwidth(torch, args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
+        print("bench.py measures one GPU: the library has no multi-GPU path "
               "(the checkpoint kernels run on one device). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
     import torch
