@@ -387,11 +387,26 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     for (int e = 0; e < 4; ++e) tpr[e] = tp[int64_t(ci) * TP_VEC + e * 64 + lane];
   };
 
+  // S' split into bf16 hi + lo in the B-operand order of X's four contraction steps: formed
+  // right after each update, where it overlaps the update's last MFMAs, so that X of the
+  // next chunk starts on its products as soon as the chunk is staged
+  bf16x8 s_hi[4], s_lo[4];
+  auto split_state = [&]() {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = S[2 * kk + (e >> 2)][e & 3];
+      split8(x, s_hi[kk], s_lo[kk]);
+    }
+  };
+
   // prologue: chunk 0 staged, chunk 1 and the first factors in flight
   fetch(0);
   stage(0);
   fetch(C);
   fetch_tp(0);
+  split_state();
   __syncthreads();
 
   for (int t0 = 0, b = 0, ci = 0; t0 < W; t0 += C, b ^= 1, ++ci) {
@@ -401,18 +416,11 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       const __bf16* sK = reinterpret_cast<const __bf16*>(bK(b));
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        bf16x8 sh, slo;
-        {
-          float x[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] = S[2 * kk + (e >> 2)][e & 3];
-          split8(x, sh, slo);
-        }
 #pragma unroll
         for (int mu = 0; mu < 2; ++mu) {
           const bf16x8 kk8 = ld_op(sK + (16 * mu + r) * SK + 32 * kk + 4 * q);
-          X[mu] = mma(kk8, slo, X[mu]);
-          X[mu] = mma(kk8, sh, X[mu]);
+          X[mu] = mma(kk8, s_lo[kk], X[mu]);
+          X[mu] = mma(kk8, s_hi[kk], X[mu]);
         }
       }
 #pragma unroll
@@ -459,6 +467,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
         S[mt] = mma(kt8, ul, S[mt] * gam);
         S[mt] = mma(kt8, uh, S[mt]);
       }
+      split_state();   // (after the last chunk: unused)
     }
 
     // ---- the next chunk into the other buffer; the one after that into registers --------
