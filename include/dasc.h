@@ -52,6 +52,10 @@ extern "C" {
 #define DASC_E_SHAPE       -2  /* shape fields inconsistent with each other      */
 #define DASC_E_WORKSPACE   -3  /* workspace smaller than dasc_refresh_workspace_bytes */
 #define DASC_E_HIP         -4  /* the HIP runtime reported an error at launch    */
+/* A device call first clears the calling thread's last HIP error (hipGetLastError), so
+ * that DASC_E_HIP reports its own launches only: check HIP's state before the call if an
+ * earlier error of the caller's matters.  Errors that happen while a kernel runs surface
+ * at the caller's next synchronisation, as for any asynchronous launch. */
 #define DASC_E_UNSUPPORTED -5  /* valid request with no kernel built for it      */
 
 /* Longest replay window dasc_refresh accepts (tokens): keeps every per-head input
