@@ -460,8 +460,8 @@ def bench_pack_restore_only(torch, args, name):
     # padded layout (App. B Scheme 1, the comparison layout): same rows moved, L * R_max
     # rows reserved per checkpoint
     del q, s
-    off_np, r_max = D.padded_geometry(sh, plan)
-    off = _i32(torch, off_np)
+    r_max = int(plan["r_max_rows"])
+    off = _i32(torch, plan["layer_off_rows"])
     ck_pad = torch.empty((sh.n_layers, n, r_max, dv), dtype=torch.float32, device="cuda")
     for _ in range(args.warmup):
         D.dasc_pack_padded(sh, states, ids, unit_row, off, ck_pad, ids)

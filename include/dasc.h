@@ -117,6 +117,8 @@ typedef struct dasc_plan_out {
   int32_t *unit_count;    /* [L*H] retained units of each (layer, head)                 */
   int32_t *off;           /* [L*H+1] first packed row of each (layer, head); off[L*H] = R */
   int32_t *layer_off;     /* [L+1] App. B offsets o_l in units: o_0 = 0, o_{l+1} = o_l + r_l */
+  int32_t *layer_off_rows; /* [L+1] the same offsets in packed rows (o_l * rows_per_unit): the
+                              layer_off_rows argument of the padded layout (App. B Scheme 1) */
   int32_t *unit_row;      /* [L*H*dk] capacity: dense row (l*H + h)*dk + c of packed row j,
                              j < R, in (layer, head, channel) order                     */
   int32_t *inv_row;       /* [L*H*dk] packed row of each dense row, -1 if omitted       */
@@ -133,6 +135,8 @@ typedef struct dasc_plan_out {
   double c_temp_rag;      /* Eq. 6: sum_l n_l / sum_l r_l (inf if nothing retained)    */
   double c_temp_pad;      /* Sec. 4.1 padded layout: sum_l n_l / (L * R_max)            */
   double layout_gain;     /* R_max / r_bar (App. B)                                     */
+  int64_t r_max_rows;     /* R_max * rows_per_unit: rows every layer reserves per checkpoint
+                             in the padded layout (App. B Scheme 1)                     */
   double c_ckpt;          /* Eq. 6 C_ckpt with per-rank bottleneck: (dense/T + conv) /
                              (C * unit bytes + conv)                                    */
   int64_t slot_bytes_rank;       /* C * unit bytes + conv_bytes (Eq. 8 b_bottleneck)    */
@@ -224,10 +228,9 @@ int dasc_restore(const dasc_shape *shape,
  * dv]; entry e < r_l of layer l holds the e-th retained row of that layer, padding is
  * not written.  Same retained values as the ragged layout; it needs L * r_max_rows
  * rows per checkpoint instead of n_rows (the layout gain of Eq. 6).
- *   layer_off_rows: device int32 [L+1], the plan's layer_off times rows per unit
- *     (1 for KDA, dk for GDN).
- *   r_max_rows: max over layers of layer_off_rows[l+1] - layer_off_rows[l]; rows a
- *     layer has past it are not written (pack) and restore as +0.0.
+ *   layer_off_rows: device int32 [L+1], dasc_plan's layer_off_rows.
+ *   r_max_rows: dasc_plan's r_max_rows; rows a layer has past it are not written
+ *     (pack) and restore as +0.0.
  *   Other arguments as dasc_pack / dasc_restore (flat addressing, no rank slices).
  * Errors: as dasc_pack / dasc_restore; DASC_E_INVAL also for r_max_rows < 1 with
  * n_rows > 0 or r_max_rows >= 2^31. */
@@ -304,7 +307,15 @@ int dasc_refresh_workspace_bytes(const dasc_shape *shape, int32_t n_req, int32_t
  *   beta: device fp32 [n_req, H, W]
  *   workspace: device, at least dasc_refresh_workspace_bytes, 16-byte aligned (may be
  *              NULL if that is 0); overlapping calls must not share one.
- * Arithmetic is fp32 with bf16 inputs widened exactly.
+ * Precision.  The state is fp32 and bf16 inputs are widened exactly.  At dk = dv = 128 the
+ * chunked WY form of Eq. 1 runs on bf16 matrix cores: every fp32 operand of a product is
+ * split into bf16 high and low parts and the product is the sum of three bf16 products
+ * (hi*hi + hi*lo + lo*hi) accumulated in fp32, about 16 significant bits per term; and
+ * each per-token log-gate is floored at -10 (a decay of at least 4.5e-5 per token, which
+ * keeps the factorised decays finite; it changes the state by at most 4.5e-5 of its
+ * magnitude per floored token).  Other shapes run a plain fp32 per-token recurrence with
+ * no floor.  Measured against an fp64 replay: within 2e-3 of each head's largest
+ * refreshed magnitude (about 1e-5 at the shapes of Sec. 5.1).
  * Errors: DASC_E_INVAL (NULL pointer, misalignment, layer out of [0, L), n_req < 1,
  * W < 1 or W > DASC_MAX_WINDOW, bad init_mode, n_pool < 1), DASC_E_SHAPE (bad shape),
  * DASC_E_WORKSPACE, DASC_E_UNSUPPORTED (dk not in {16, 32, 64, 128} or dv > 256),
@@ -317,7 +328,9 @@ int dasc_refresh(const dasc_shape *shape, int32_t layer, const int32_t *inv_row,
 
 /* ---- Load with refresh, fused (Sec. 4.2: restore, then DASC-WR) ----------- */
 
-/* One launch doing what dasc_restore followed by dasc_refresh does for one layer:
+/* What dasc_restore followed by dasc_refresh does for one layer, without the separate
+ * restore pass (one launch for KDA heads; GDN heads take two, the state-independent
+ * factor launch of dasc_refresh and then the fused recurrence):
  * for each request i < n_req, the rows of layer `layer` of states[dst_slot[i]] receive
  *   - omitted rows of heads that have any (KDA rows; GDN whole heads): S'_W of the
  *     replay above, started from the restored head (kept rows taken from checkpoint
@@ -332,7 +345,7 @@ int dasc_refresh(const dasc_shape *shape, int32_t layer, const int32_t *inv_row,
  *   states, dst_slot: as states, slot in dasc_refresh (the pool need not hold the
  *   restored state beforehand).
  *   k, v, g, beta, W, init_mode, workspace: as in dasc_refresh.
- * Built for dk = dv = 128 (the shapes of Sec. 5.1).
+ * Built for dk = dv = 128 (the shapes of Sec. 5.1); precision as in dasc_refresh.
  * Errors: those of dasc_restore and dasc_refresh; DASC_E_UNSUPPORTED unless
  * dk = dv = 128. */
 int dasc_restore_refresh(const dasc_shape *shape, int32_t layer,

@@ -125,7 +125,9 @@ def build_plan(g: np.ndarray, arch: str, n_layers: int, n_heads: int, dk: int, d
     g: [L, H, dk] for KDA, [L, H] for GDN.  Returns a dict of numpy arrays/scalars:
       keep[L,H(,dk)] bool, horizon, unit_count[L,H] (units kept per head),
       off[L*H+1] (row offsets of each (l,h) block in the packed buffer),
-      layer_off[L+1] (App. B o_l, in units), unit_row[R] (dense row of packed row j),
+      layer_off[L+1] (App. B o_l, in units), layer_off_rows[L+1] (the same in rows),
+      r_max_rows (rows each layer reserves in the padded layout of App. B Scheme 1),
+      unit_row[R] (dense row of packed row j),
       inv_row[L*H*dk] (packed row of dense row, -1 if omitted), n_rows R,
       n_units, rows_per_unit, w_units (Eq. 7 per unit, 0 for kept units), w_replay,
       slice_units C, slice_rows, rank_begin[T+1] (rows), send[T,T] (units),
@@ -216,9 +218,14 @@ def build_plan(g: np.ndarray, arch: str, n_layers: int, n_heads: int, dk: int, d
     rag_rank = C * unit_bytes
     c_ckpt = (dense_rank + conv_bytes) / (rag_rank + conv_bytes) if (rag_rank + conv_bytes) else inf
 
+    # App. B Scheme 1: every layer reserves the largest layer's retained rows
+    layer_off_rows = layer_off * rows_per_unit
+    r_max_rows = r_max * rows_per_unit
+
     return {
         "arch": arch, "g": g, "horizon": Hs, "keep": keep, "unit_count": unit_count,
-        "off": off, "layer_off": layer_off, "unit_row": unit_row, "inv_row": inv_row,
+        "off": off, "layer_off": layer_off, "layer_off_rows": layer_off_rows,
+        "r_max_rows": r_max_rows, "unit_row": unit_row, "inv_row": inv_row,
         "n_rows": n_rows, "n_units": n_units, "rows_per_unit": rows_per_unit,
         "w_units": w_units, "w_replay": w_replay,
         "slice_units": C, "slice_rows": C * rows_per_unit, "rank_begin": rank_begin, "send": send,

@@ -15,6 +15,7 @@ from .dasc import (  # noqa: F401
     dasc_pack_q8,
     dasc_plan,
     dasc_refresh,
+    dasc_refresh_select,
     dasc_refresh_workspace_bytes,
     dasc_restore,
     dasc_restore_padded,
@@ -22,5 +23,4 @@ from .dasc import (  # noqa: F401
     dasc_restore_refresh,
     dasc_static_log_decay,
     dasc_tp_permutation,
-    padded_geometry,
 )

@@ -26,12 +26,15 @@ DASC_KEEP_TOPK_PER_HEAD = 1
 DASC_KEEP_TOPK_PER_LAYER = 2
 DASC_INIT_RESTORED = 0
 DASC_INIT_ZERO = 1
+DASC_REFRESH_KERNEL_AUTO = 0
+DASC_REFRESH_KERNEL_COLUMN = 1
+DASC_REFRESH_KERNEL_CHANNEL_WY = 2
 
 EXPORTED = (
     "dasc_static_log_decay", "dasc_plan", "dasc_matched_slots", "dasc_strerror",
     "dasc_pack", "dasc_restore", "dasc_pack_q8", "dasc_restore_q8",
     "dasc_refresh_workspace_bytes", "dasc_refresh", "dasc_restore_refresh",
-    "dasc_tp_permutation", "dasc_pack_padded", "dasc_restore_padded",
+    "dasc_tp_permutation", "dasc_pack_padded", "dasc_restore_padded", "dasc_refresh_select",
 )
 
 
@@ -50,12 +53,14 @@ class PlanOut(C.Structure):
     _fields_ = [
         ("keep", C.POINTER(C.c_uint8)), ("horizon", C.POINTER(C.c_double)),
         ("unit_count", C.POINTER(C.c_int32)), ("off", C.POINTER(C.c_int32)),
-        ("layer_off", C.POINTER(C.c_int32)), ("unit_row", C.POINTER(C.c_int32)),
+        ("layer_off", C.POINTER(C.c_int32)), ("layer_off_rows", C.POINTER(C.c_int32)),
+        ("unit_row", C.POINTER(C.c_int32)),
         ("inv_row", C.POINTER(C.c_int32)), ("w_units", C.POINTER(C.c_int32)),
         ("rank_begin", C.POINTER(C.c_int32)), ("send", C.POINTER(C.c_int64)),
         ("n_rows", C.c_int64), ("n_units", C.c_int64), ("rows_per_unit", C.c_int32),
         ("w_replay", C.c_int32), ("slice_units", C.c_int64), ("slice_rows", C.c_int64),
         ("c_temp_rag", C.c_double), ("c_temp_pad", C.c_double), ("layout_gain", C.c_double),
+        ("r_max_rows", C.c_int64),
         ("c_ckpt", C.c_double), ("slot_bytes_rank", C.c_int64), ("dense_slot_bytes_rank", C.c_int64),
     ]
 
@@ -98,6 +103,8 @@ def _load() -> C.CDLL:
         "dasc_restore_q8": [C.POINTER(Shape), P, P, I64, P, I64, P, P, I64, P, I32, P],
         "dasc_refresh_workspace_bytes": [C.POINTER(Shape), I32, I32, C.POINTER(C.c_size_t)],
         "dasc_refresh": [C.POINTER(Shape), I32, P, P, I64, P, P, P, P, P, I32, I32, I32, P, SZ, P],
+        "dasc_refresh_select": [C.POINTER(Shape), I32, P, P, I64, P, P, P, P, P, I32, I32, I32, P, SZ,
+                                I32, P],
         "dasc_restore_refresh": [C.POINTER(Shape), I32, P, I64, P, I32, I64, I64, P, P, I64, P,
                                  P, P, P, P, I32, I32, I32, P, SZ, P],
     }

@@ -117,8 +117,6 @@ __device__ __forceinline__ void pack_body(
   }
 }
 
-// Restore body; PADDED selects the padded layout, where the slice of a packed row is
-// the layer of its dense row (known per block unless the block straddles two layers).
 template <int VPR_LOG2>
 __global__ __launch_bounds__(kThreads) void pack_kernel(
     const f32x4* __restrict__ states, int64_t n_pool, int64_t rows_state,
@@ -140,6 +138,8 @@ __global__ __launch_bounds__(kThreads) void pack_padded_kernel(
                       dst_slot, slice_rows, n_ranks, blocks_per_slice, rpb, vpr_rt, slice_begin);
 }
 
+// Restore body; PADDED selects the padded layout, where the slice of a packed row is
+// the layer of its dense row (known per block unless the block straddles two layers).
 template <int VPR_LOG2, bool PADDED>
 __device__ __forceinline__ void restore_body(
     const f32x4* __restrict__ ckpt, int64_t n_ckpt_slots, const int32_t* __restrict__ src_slot,

@@ -154,12 +154,14 @@ extern "C" int dasc_plan(const dasc_plan_desc* desc, const double* g, dasc_plan_
   std::vector<int64_t> r_layer(L, 0);
   for (int64_t l = 0; l < L; ++l)
     for (int64_t h = 0; h < H; ++h) r_layer[l] += ucount[l * H + h];
-  if (out->layer_off) {
+  if (out->layer_off || out->layer_off_rows) {
     int64_t acc = 0;
-    out->layer_off[0] = 0;
+    if (out->layer_off) out->layer_off[0] = 0;
+    if (out->layer_off_rows) out->layer_off_rows[0] = 0;
     for (int64_t l = 0; l < L; ++l) {
       acc += r_layer[l];
-      out->layer_off[l + 1] = static_cast<int32_t>(acc);
+      if (out->layer_off) out->layer_off[l + 1] = static_cast<int32_t>(acc);
+      if (out->layer_off_rows) out->layer_off_rows[l + 1] = static_cast<int32_t>(acc * rows_per_unit);
     }
   }
 
@@ -205,6 +207,7 @@ extern "C" int dasc_plan(const dasc_plan_desc* desc, const double* g, dasc_plan_
                     ? static_cast<double>(dense_rank + desc->conv_bytes) /
                           static_cast<double>(rag_rank + desc->conv_bytes)
                     : inf;
+  out->r_max_rows = r_max * rows_per_unit;
   out->slot_bytes_rank = rag_rank + desc->conv_bytes;
   out->dense_slot_bytes_rank = dense_rank + desc->conv_bytes;
 

@@ -17,10 +17,9 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
-#include <cstdlib>
-#include <cstring>
 
 #include "dasc.h"
+#include "dasc_testing.h"
 #include "launch_common.h"
 #include "refresh_kernels.h"
 
@@ -114,8 +113,7 @@ void launch_column(bool per_channel, dim3 grid, dim3 block, size_t lds, hipStrea
                        L, inv_row, states, n_pool, slot, k, v, g, beta, W, init_zero);
 }
 
-// Does this shape take the two-launch scalar-gate GDN kernel (unless the channel-wise
-// kernel is forced with DASC_REFRESH_KERNEL)?
+// Does this shape take the two-launch scalar-gate GDN kernel?
 bool uses_gdn_factors(const dasc_shape* shape) {
   return shape->arch == DASC_ARCH_GDN && dasc::refresh_wy_supported(shape->dk, shape->dv);
 }
@@ -134,55 +132,57 @@ extern "C" int dasc_refresh_workspace_bytes(const dasc_shape* shape, int32_t n_r
   return DASC_OK;
 }
 
-extern "C" int dasc_refresh(const dasc_shape* shape, int32_t layer, const int32_t* inv_row,
-                            float* states, int64_t n_pool, const int32_t* slot,
-                            const uint16_t* k, const uint16_t* v, const float* g,
-                            const float* beta, int32_t n_req, int32_t W, int32_t init_mode,
-                            void* workspace, size_t workspace_bytes, dasc_stream_t stream) {
+namespace dasc {
+
+// dasc_refresh with an explicit kernel choice (DASC_REFRESH_KERNEL_*): AUTO takes the
+// chunked MFMA kernels at dk = dv = 128 (the scalar-gate one for GDN heads) and the
+// per-column fp32 kernel for every other shape.
+int refresh_impl(const dasc_shape* shape, int32_t layer, const int32_t* inv_row, float* states,
+                 int64_t n_pool, const int32_t* slot, const uint16_t* k, const uint16_t* v,
+                 const float* g, const float* beta, int32_t n_req, int32_t W, int32_t init_mode,
+                 void* workspace, size_t workspace_bytes, int32_t kernel, dasc_stream_t stream) {
   if (!shape) return DASC_E_INVAL;
   if (!dasc::valid_shape(shape) || shape->dv % 4 != 0) return DASC_E_SHAPE;
   if (layer < 0 || layer >= shape->n_layers || n_req < 1 || W < 1 || W > DASC_MAX_WINDOW ||
       n_pool < 1)
     return DASC_E_INVAL;
   if (init_mode != DASC_INIT_RESTORED && init_mode != DASC_INIT_ZERO) return DASC_E_INVAL;
+  if (kernel != DASC_REFRESH_KERNEL_AUTO && kernel != DASC_REFRESH_KERNEL_COLUMN &&
+      kernel != DASC_REFRESH_KERNEL_CHANNEL_WY)
+    return DASC_E_INVAL;
   if (!inv_row || !states || !slot || !k || !v || !g || !beta) return DASC_E_INVAL;
   if (!dasc::aligned16(states) || !dasc::aligned16(k) || !dasc::aligned16(v)) return DASC_E_INVAL;
-  size_t need = 0;
-  int rc = dasc_refresh_workspace_bytes(shape, n_req, W, &need);
-  if (rc != DASC_OK) return rc;
-  if (workspace_bytes < need || (need > 0 && !workspace)) return DASC_E_WORKSPACE;
-  if (need > 0 && !dasc::aligned16(workspace)) return DASC_E_INVAL;
   const int dk = shape->dk, dv = shape->dv;
   if (dv > 256) return DASC_E_UNSUPPORTED;
+  if (kernel == DASC_REFRESH_KERNEL_CHANNEL_WY && !dasc::refresh_wy_supported(dk, dv))
+    return DASC_E_UNSUPPORTED;
+  const bool gdn_factors = kernel == DASC_REFRESH_KERNEL_AUTO && uses_gdn_factors(shape);
+  const size_t need =
+      gdn_factors ? dasc::gdn_factor_workspace_bytes(n_req, shape->n_heads, W) : 0;
+  if (workspace_bytes < need || (need > 0 && !workspace)) return DASC_E_WORKSPACE;
+  if (need > 0 && !dasc::aligned16(workspace)) return DASC_E_INVAL;
   if (2 * int64_t(n_req) * shape->n_heads > INT32_MAX) return DASC_E_INVAL;  // GDN: 2 blocks a head
 
   const bool per_channel = shape->arch == DASC_ARCH_KDA;
-  const int threads = ((dv + 63) / 64) * 64;
-  const dim3 grid(unsigned(n_req) * unsigned(shape->n_heads));
-  const size_t lds = size_t(kTile) * dv * sizeof(float);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int zero = init_mode == DASC_INIT_ZERO;
   (void)hipGetLastError();
-  // The chunked MFMA kernel serves dk = dv = 128; every other shape, or an explicit
-  // DASC_REFRESH_KERNEL=column, takes the per-column fp32 kernel.  GDN heads at that
-  // shape take the scalar-gate kernel unless DASC_REFRESH_KERNEL=wy asks for the
-  // channel-wise one (both exist for comparison).
-  const char* pick = std::getenv("DASC_REFRESH_KERNEL");
-  const bool force_column = pick && std::strcmp(pick, "column") == 0;
-  const bool force_wy = pick && std::strcmp(pick, "wy") == 0;
-  if (!force_column && !force_wy && uses_gdn_factors(shape)) {
+  if (gdn_factors) {
     if (dasc::gdn_factor_blocks(n_req, shape->n_heads, W) > INT32_MAX) return DASC_E_INVAL;
     dasc::launch_refresh_wy_gdn(n_req, shape->n_heads, shape->n_qk_heads, layer,
                                 shape->n_layers, inv_row, states, n_pool, slot, k, v, g, beta, W,
                                 zero, workspace, st);
     return dasc::launch_status();
   }
-  if (!force_column && dasc::refresh_wy_supported(dk, dv)) {
+  if (kernel != DASC_REFRESH_KERNEL_COLUMN && dasc::refresh_wy_supported(dk, dv)) {
     dasc::launch_refresh_wy(per_channel, n_req, shape->n_heads, shape->n_qk_heads, layer,
                             shape->n_layers, inv_row, states, n_pool, slot, k, v, g, beta, W,
                             zero, st);
     return dasc::launch_status();
   }
+  const int threads = ((dv + 63) / 64) * 64;
+  const dim3 grid(unsigned(n_req) * unsigned(shape->n_heads));
+  const size_t lds = size_t(kTile) * dv * sizeof(float);
   switch (dk) {
 #define DASC_DK(D)                                                                              \
   case D:                                                                                       \
@@ -195,6 +195,28 @@ extern "C" int dasc_refresh(const dasc_shape* shape, int32_t layer, const int32_
     default: return DASC_E_UNSUPPORTED;
   }
   return dasc::launch_status();
+}
+
+}  // namespace dasc
+
+extern "C" int dasc_refresh(const dasc_shape* shape, int32_t layer, const int32_t* inv_row,
+                            float* states, int64_t n_pool, const int32_t* slot,
+                            const uint16_t* k, const uint16_t* v, const float* g,
+                            const float* beta, int32_t n_req, int32_t W, int32_t init_mode,
+                            void* workspace, size_t workspace_bytes, dasc_stream_t stream) {
+  return dasc::refresh_impl(shape, layer, inv_row, states, n_pool, slot, k, v, g, beta, n_req, W,
+                            init_mode, workspace, workspace_bytes, DASC_REFRESH_KERNEL_AUTO,
+                            stream);
+}
+
+extern "C" int dasc_refresh_select(const dasc_shape* shape, int32_t layer, const int32_t* inv_row,
+                                   float* states, int64_t n_pool, const int32_t* slot,
+                                   const uint16_t* k, const uint16_t* v, const float* g,
+                                   const float* beta, int32_t n_req, int32_t W, int32_t init_mode,
+                                   void* workspace, size_t workspace_bytes, int32_t kernel,
+                                   dasc_stream_t stream) {
+  return dasc::refresh_impl(shape, layer, inv_row, states, n_pool, slot, k, v, g, beta, n_req, W,
+                            init_mode, workspace, workspace_bytes, kernel, stream);
 }
 
 extern "C" int dasc_restore_refresh(const dasc_shape* shape, int32_t layer, const float* ckpt,
@@ -230,11 +252,8 @@ extern "C" int dasc_restore_refresh(const dasc_shape* shape, int32_t layer, cons
   if (2 * int64_t(n_req) * shape->n_heads > INT32_MAX) return DASC_E_INVAL;  // GDN: 2 blocks a head
   if (n_rows == 0) slice_rows = 1;  // nothing is read; keeps the divisor non-zero
   (void)hipGetLastError();
-  // GDN heads take the scalar-gate kernel, as in dasc_refresh (DASC_REFRESH_KERNEL=wy
-  // selects the channel-wise one)
-  const char* pick = std::getenv("DASC_REFRESH_KERNEL");
-  const bool force_wy = pick && std::strcmp(pick, "wy") == 0;
-  if (uses_gdn_factors(shape) && !force_wy) {
+  // GDN heads take the scalar-gate kernel, as in dasc_refresh
+  if (uses_gdn_factors(shape)) {
     if (dasc::gdn_factor_blocks(n_req, shape->n_heads, W) > INT32_MAX) return DASC_E_INVAL;
     dasc::launch_restore_refresh_wy_gdn(n_req, shape->n_heads, shape->n_qk_heads, layer,
                                         shape->n_layers, ckpt, n_ckpt_slots, src_slot, slice_rows,

@@ -6,7 +6,16 @@
 #include <cstddef>
 #include <cstdint>
 
+#include "dasc.h"
+
 namespace dasc {
+
+// The body of dasc_refresh with an explicit kernel choice (DASC_REFRESH_KERNEL_*, see
+// dasc_testing.h); validates every argument before it launches anything.
+int refresh_impl(const dasc_shape* shape, int32_t layer, const int32_t* inv_row, float* states,
+                 int64_t n_pool, const int32_t* slot, const uint16_t* k, const uint16_t* v,
+                 const float* g, const float* beta, int32_t n_req, int32_t W, int32_t init_mode,
+                 void* workspace, size_t workspace_bytes, int32_t kernel, dasc_stream_t stream);
 
 // Chunkwise WY-form kernel on bf16 MFMA; built for dk = dv = 128 only.
 bool refresh_wy_supported(int dk, int dv);

@@ -82,7 +82,8 @@ def dasc_plan(shape: Shape, g_static, keep_mode: str = "threshold", keep_k: int 
     arr = {
         "keep": np.zeros(nu, np.uint8), "horizon": np.zeros(nu, np.float64),
         "unit_count": np.zeros(L * H, np.int32), "off": np.zeros(L * H + 1, np.int32),
-        "layer_off": np.zeros(L + 1, np.int32), "unit_row": np.zeros(rows, np.int32),
+        "layer_off": np.zeros(L + 1, np.int32), "layer_off_rows": np.zeros(L + 1, np.int32),
+        "unit_row": np.zeros(rows, np.int32),
         "inv_row": np.zeros(rows, np.int32), "w_units": np.zeros(nu, np.int32),
         "rank_begin": np.zeros(T + 1, np.int32), "send": np.zeros(T * T, np.int64),
     }
@@ -98,7 +99,7 @@ def dasc_plan(shape: Shape, g_static, keep_mode: str = "threshold", keep_k: int 
         "keep": arr["keep"].astype(bool).reshape(unit_shape),
         "horizon": arr["horizon"].reshape(unit_shape),
         "unit_count": arr["unit_count"].reshape(L, H),
-        "off": arr["off"], "layer_off": arr["layer_off"],
+        "off": arr["off"], "layer_off": arr["layer_off"], "layer_off_rows": arr["layer_off_rows"],
         "unit_row": arr["unit_row"][: res["n_rows"]].copy(),
         "inv_row": arr["inv_row"], "w_units": arr["w_units"].reshape(unit_shape),
         "rank_begin": arr["rank_begin"], "send": arr["send"].reshape(T, T),
@@ -192,16 +193,11 @@ def dasc_restore(shape: Shape, ckpt, src_slot, inv_row, states, dst_slot, n_rows
         _stream(stream)), "dasc_restore")
 
 
-def padded_geometry(shape: Shape, plan: dict) -> tuple[np.ndarray, int]:
-    """(layer_off_rows [L+1] int32, r_max_rows) of the padded layout for a plan."""
-    rpu = int(plan["rows_per_unit"])
-    off = (np.asarray(plan["layer_off"], dtype=np.int64) * rpu).astype(np.int32)
-    return off, int(np.diff(off).max()) if off.size > 1 else 0
-
-
 def dasc_pack_padded(shape: Shape, states, src_slot, unit_row, layer_off_rows, ckpt, dst_slot,
                      stream=None) -> None:
-    """App. B Scheme 1 pack; ckpt is [L, n_slots, r_max_rows, dv] float32."""
+    """App. B Scheme 1 pack; ckpt is [L, n_slots, r_max_rows, dv] float32, with
+    layer_off_rows and r_max_rows from dasc_plan (the device copy of its layer_off_rows,
+    and ckpt's third dimension)."""
     import torch
 
     L, n_slots, r_max = ckpt.shape[0], ckpt.shape[1], ckpt.shape[2]
@@ -280,28 +276,31 @@ def dasc_refresh_workspace_bytes(shape: Shape, n_req: int, W: int) -> int:
 
 
 def _workspace(shape: Shape, n_req: int, W: int, workspace, device, stream):
-    """(pointer, bytes) of the refresh workspace: the caller's uint8 device tensor, or one
-    drawn from torch's allocator when none is given and the call needs it.  A drawn one is
-    tied to the launch stream, so torch does not hand it out again before the launch ends."""
+    """(tensor, pointer, bytes) of the refresh workspace: the caller's uint8 device tensor,
+    or one drawn from torch's allocator when none is given and the call needs it.  A drawn
+    one is allocated on the launch stream itself, so that torch's allocator orders its
+    reuse after this call's kernels and the block is never one that work still queued on
+    another stream is using.  The caller keeps the returned tensor alive until the launch
+    has been enqueued."""
     import torch
 
     if workspace is None:
         need = dasc_refresh_workspace_bytes(shape, n_req, W)
         if need == 0:
-            return None, 0
-        workspace = torch.empty(need, dtype=torch.uint8, device=device)
-        if stream is not None:
-            workspace.record_stream(stream)
-    return _dev(workspace, torch.uint8, "workspace"), workspace.numel()
+            return None, None, 0
+        if stream is None:
+            workspace = torch.empty(need, dtype=torch.uint8, device=device)
+        else:
+            with torch.cuda.stream(stream):
+                workspace = torch.empty(need, dtype=torch.uint8, device=device)
+    return workspace, _dev(workspace, torch.uint8, "workspace"), workspace.numel()
 
 
-def dasc_refresh(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta, W: int,
-                 init_mode: str = "restored", workspace=None, stream=None) -> None:
-    """Refresh one layer's omitted units for every request in `slot`.
+REFRESH_KERNEL = {"auto": _lib.DASC_REFRESH_KERNEL_AUTO, "column": _lib.DASC_REFRESH_KERNEL_COLUMN,
+                  "channel_wy": _lib.DASC_REFRESH_KERNEL_CHANNEL_WY}
 
-    k [n_req, Hqk, W, dk] and v [n_req, H, W, dv] are bfloat16 device tensors; g is
-    [n_req, H, W, dk] (KDA) or [n_req, H, W] (GDN) and beta [n_req, H, W], float32.
-    """
+
+def _refresh_args(shape: Shape, inv_row, states, slot, k, v, g, beta, W: int):
     import torch
 
     n_req, H, dk, dv = slot.numel(), shape.n_heads, shape.dk, shape.dv
@@ -311,13 +310,40 @@ def dasc_refresh(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta,
     _need(v, n_req * H * W * dv, "v")
     _need(g, n_req * H * W * (dk if shape.arch == "kda" else 1), "g")
     _need(beta, n_req * H * W, "beta")
-    ws_ptr, ws_bytes = _workspace(shape, n_req, W, workspace, states.device, stream)
-    _check(LIB.dasc_refresh(
-        C.byref(shape.c()), layer, _dev(inv_row, torch.int32, "inv_row"),
-        _dev(states, torch.float32, "states"), states.shape[0], _dev(slot, torch.int32, "slot"),
-        _dev(k, torch.bfloat16, "k"), _dev(v, torch.bfloat16, "v"),
-        _dev(g, torch.float32, "g"), _dev(beta, torch.float32, "beta"),
-        slot.numel(), W, INIT[init_mode], ws_ptr, ws_bytes, _stream(stream)), "dasc_refresh")
+    return (_dev(inv_row, torch.int32, "inv_row"), _dev(states, torch.float32, "states"),
+            states.shape[0], _dev(slot, torch.int32, "slot"), _dev(k, torch.bfloat16, "k"),
+            _dev(v, torch.bfloat16, "v"), _dev(g, torch.float32, "g"),
+            _dev(beta, torch.float32, "beta"), n_req)
+
+
+def dasc_refresh(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta, W: int,
+                 init_mode: str = "restored", workspace=None, stream=None) -> None:
+    """Refresh one layer's omitted units for every request in `slot`.
+
+    k [n_req, Hqk, W, dk] and v [n_req, H, W, dv] are bfloat16 device tensors; g is
+    [n_req, H, W, dk] (KDA) or [n_req, H, W] (GDN) and beta [n_req, H, W], float32.
+    """
+    a = _refresh_args(shape, inv_row, states, slot, k, v, g, beta, W)
+    ws, ws_ptr, ws_bytes = _workspace(shape, a[-1], W, workspace, states.device, stream)
+    _check(LIB.dasc_refresh(C.byref(shape.c()), layer, *a, W,
+                            INIT[init_mode], ws_ptr, ws_bytes, _stream(stream)), "dasc_refresh")
+    del ws
+
+
+def dasc_refresh_select(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta, W: int,
+                        kernel: str, init_mode: str = "restored", workspace=None,
+                        stream=None) -> None:
+    """dasc_refresh on a named kernel ("auto", "column" or "channel_wy"), for tests and
+    comparisons (dasc_testing.h)."""
+    a = _refresh_args(shape, inv_row, states, slot, k, v, g, beta, W)
+    if kernel == "auto":
+        ws, ws_ptr, ws_bytes = _workspace(shape, a[-1], W, workspace, states.device, stream)
+    else:
+        ws, ws_ptr, ws_bytes = None, None, 0
+    _check(LIB.dasc_refresh_select(C.byref(shape.c()), layer, *a, W,
+                                   INIT[init_mode], ws_ptr, ws_bytes, REFRESH_KERNEL[kernel],
+                                   _stream(stream)), "dasc_refresh_select")
+    del ws
 
 
 def dasc_restore_refresh(shape: Shape, layer: int, ckpt, src_slot, inv_row, states, dst_slot,
@@ -341,7 +367,7 @@ def dasc_restore_refresh(shape: Shape, layer: int, ckpt, src_slot, inv_row, stat
     _need(v, n_req * H * W * dv, "v")
     _need(g, n_req * H * W * (dk if shape.arch == "kda" else 1), "g")
     _need(beta, n_req * H * W, "beta")
-    ws_ptr, ws_bytes = _workspace(shape, n_req, W, workspace, states.device, stream)
+    ws, ws_ptr, ws_bytes = _workspace(shape, n_req, W, workspace, states.device, stream)
     _check(LIB.dasc_restore_refresh(
         C.byref(shape.c()), layer, _dev(ckpt, torch.float32, "ckpt"), n_slots,
         _dev(src_slot, torch.int32, "src_slot"), n_ranks, slice_rows, n_rows,
@@ -350,3 +376,4 @@ def dasc_restore_refresh(shape: Shape, layer: int, ckpt, src_slot, inv_row, stat
         _dev(k, torch.bfloat16, "k"), _dev(v, torch.bfloat16, "v"),
         _dev(g, torch.float32, "g"), _dev(beta, torch.float32, "beta"),
         n_req, W, INIT[init_mode], ws_ptr, ws_bytes, _stream(stream)), "dasc_restore_refresh")
+    del ws

@@ -12,20 +12,24 @@ from paper_2608_30386_amd import _lib
 from paper_2608_30386_amd._lib import LIB, Shape, PlanDesc, PlanOut
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "dasc.h")
+HEADERS = [os.path.join(ROOT, "include", f) for f in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if f.endswith(".h")]
 
 FAKE = C.c_void_p(0x10000)       # aligned, never dereferenced: validation fails first
 FAKE_ODD = C.c_void_p(0x10004)   # not 16-byte aligned
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    return sorted(set(re.findall(r"^(?:int|const char \*)\s*(dasc_\w+)\s*\(", text, re.M)))
+    names = set()
+    for h in HEADERS:
+        text = open(h).read()
+        names |= set(re.findall(r"^(?:int|const char \*)\s*(dasc_\w+)\s*\(", text, re.M))
+    return sorted(names)
 
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 15
     assert set(names) == set(_lib.EXPORTED)
     lib = C.CDLL(_lib.LIB_PATH)
     for n in names:
@@ -198,6 +202,55 @@ def test_refresh_argument_errors():
     assert LIB.dasc_refresh_workspace_bytes(C.byref(kda()), 1, 0, C.byref(need)) == E.DASC_E_INVAL
     assert LIB.dasc_refresh_workspace_bytes(C.byref(kda()), 2, 64, C.byref(need)) == E.DASC_OK
     assert need.value == 0
+
+
+def select(shape, kernel, **kw):
+    p = dict(inv=FAKE, states=FAKE, slot=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE)
+    p.update(kw.pop("ptrs", {}))
+    ws, ws_bytes = kw.pop("ws", None), kw.pop("ws_bytes", 0)
+    W, n_req = kw.pop("W", 8), kw.pop("n_req", 1)
+    return LIB.dasc_refresh_select(C.byref(shape) if shape is not None else None, 0, p["inv"],
+                                   p["states"], 1, p["slot"], p["k"], p["v"], p["g"], p["beta"],
+                                   n_req, W, 0, ws, ws_bytes, kernel, None)
+
+
+def test_refresh_select_argument_errors():
+    # the kernel choice is an explicit argument (no process-wide switch)
+    E = _lib
+    assert select(kda(), 3) == E.DASC_E_INVAL                          # unknown kernel
+    assert select(kda(), -1) == E.DASC_E_INVAL
+    assert select(None, E.DASC_REFRESH_KERNEL_COLUMN) == E.DASC_E_INVAL
+    # the channel-wise chunked kernel exists for dk = dv = 128 only
+    assert select(kda(dk=16, dv=16), E.DASC_REFRESH_KERNEL_CHANNEL_WY) == E.DASC_E_UNSUPPORTED
+    assert select(kda(dk=64, dv=128), E.DASC_REFRESH_KERNEL_CHANNEL_WY) == E.DASC_E_UNSUPPORTED
+    # AUTO on GDN heads at 128 needs the factor workspace, like dasc_refresh
+    gdn = Shape(_lib.DASC_ARCH_GDN, 1, 4, 2, 128, 128)
+    assert select(gdn, E.DASC_REFRESH_KERNEL_AUTO, W=64, n_req=2) == E.DASC_E_WORKSPACE
+    for name in ("inv", "states", "slot", "k", "v", "g", "beta"):
+        assert select(kda(), E.DASC_REFRESH_KERNEL_COLUMN, ptrs={name: None}) == E.DASC_E_INVAL
+    assert os.path.basename(HEADERS[0]) == "dasc.h" and len(HEADERS) >= 2
+    for src in ("refresh.hip", "refresh_wy.hip", "refresh_wy_gdn.hip"):
+        text = open(os.path.join(ROOT, "paper_2608_30386_amd", "csrc", src)).read()
+        assert "getenv" not in text, src
+
+
+def test_plan_padded_geometry_fields():
+    # App. B Scheme 1 geometry comes out of the planner: per-layer offsets in rows and
+    # the rows every layer reserves; a NULL layer_off_rows member is skipped
+    E = _lib
+    sh = Shape(_lib.DASC_ARCH_GDN, 3, 4, 2, 8, 4)
+    keep = np.array([[1, 0, 0, 1], [0, 0, 0, 0], [1, 1, 1, 0]], bool)
+    g = np.where(keep, np.log(1e-3) / 1000.0, np.log(1e-3) / 2.0).reshape(-1)
+    out = PlanOut()
+    rows = np.full(4, -9, np.int32)
+    out.layer_off_rows = rows.ctypes.data_as(C.POINTER(C.c_int32))
+    desc = PlanDesc(sh, 0, 0, 16, 1, 1e-3, 0)
+    assert LIB.dasc_plan(C.byref(desc), g.ctypes.data, C.byref(out)) == E.DASC_OK
+    np.testing.assert_array_equal(rows, [0, 16, 16, 40])                 # 2, 0, 3 heads of 8 rows
+    assert out.r_max_rows == 24 and out.n_rows == 40
+    out2 = PlanOut()
+    assert LIB.dasc_plan(C.byref(desc), g.ctypes.data, C.byref(out2)) == E.DASC_OK
+    assert out2.r_max_rows == 24
 
 
 def test_gdn_refresh_workspace():

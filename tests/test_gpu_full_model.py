@@ -66,7 +66,7 @@ def test_full_model_pack_restore_all_layouts():
         assert np.array_equal(got.view(np.uint32), want[0].view(np.uint32)), f"restore_q8 {i} differs"
     del q, s
 
-    off_rows, r_max = D.padded_geometry(sh, lib)
+    off_rows, r_max = lib["layer_off_rows"], int(lib["r_max_rows"])
     ck_pad = torch.full((sh.n_layers, n, r_max, dv), -5.0, device="cuda")
     announce(f"pack_padded / restore_padded n={n} r_max={r_max}")
     D.dasc_pack_padded(sh, states, dev_i32(src), dev_i32(lib["unit_row"]), dev_i32(off_rows), ck_pad,

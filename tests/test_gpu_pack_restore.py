@@ -169,7 +169,7 @@ def _padded_roundtrip(sh, plan, states_np, src, dst, n_slots):
 
     n_pool, rows, dv, L = states_np.shape[0], sh.rows, sh.dv, sh.n_layers
     R = int(plan["n_rows"])
-    off, r_max = D.padded_geometry(sh, plan)
+    off, r_max = plan["layer_off_rows"], int(plan["r_max_rows"])
     rpu = int(plan["rows_per_unit"])
     words = states_np.reshape(n_pool, rows, dv).view(np.uint32)
     st = dev(states_np.reshape(n_pool, L, sh.n_heads, sh.dk, dv))

@@ -34,15 +34,21 @@ def restored_states(wl, plan, n_req, layer=0, salt=0):
     return np.ascontiguousarray(full)
 
 
-def run_refresh(sh, pool, layer, inv_row, inp, W, init="restored", slots=None):
+def run_refresh(sh, pool, layer, inv_row, inp, W, init="restored", slots=None, kernel=None):
+    """dasc_refresh (or, with `kernel`, dasc_refresh_select on that kernel) on a copy of
+    the pool; returns the pool after the call."""
     import torch
 
     n_req = inp["k"].shape[0]
     states = dev(pool)
     slots = list(range(n_req)) if slots is None else slots
-    announce(f"refresh {sh} layer={layer} n_req={n_req} W={W} init={init}")
-    D.dasc_refresh(sh, layer, dev_i32(inv_row), states, dev_i32(slots), dev_bf16(inp["k"]),
-                   dev_bf16(inp["v"]), dev(inp["g"]), dev(inp["beta"]), W, init)
+    announce(f"refresh {sh} layer={layer} n_req={n_req} W={W} init={init} kernel={kernel}")
+    args = (sh, layer, dev_i32(inv_row), states, dev_i32(slots), dev_bf16(inp["k"]),
+            dev_bf16(inp["v"]), dev(inp["g"]), dev(inp["beta"]), W)
+    if kernel is None:
+        D.dasc_refresh(*args, init)
+    else:
+        D.dasc_refresh_select(*args, kernel, init)
     torch.cuda.synchronize()
     return states.cpu().numpy()
 
@@ -204,7 +210,7 @@ def test_chunked_kernel_ragged_and_strong_decay(arch, W, g_lo):
         announce(f"chunked {arch} W={W} g_lo={g_lo} init={init} max rel err {err:.2e}")
 
 
-def test_chunked_and_column_kernels_agree(monkeypatch):
+def test_chunked_and_column_kernels_agree():
     wl = WORKLOADS["kimi_layer"]
     lib, _ = plans(wl)
     sh = shape_of(wl)
@@ -212,8 +218,7 @@ def test_chunked_and_column_kernels_agree(monkeypatch):
     pool = restored_states(wl, lib, n_req)
     inp = refresh_inputs(wl, 160, log_lambda(wl)[0], n_req=n_req)
     a = run_refresh(sh, pool, 0, lib["inv_row"], inp, 160)
-    monkeypatch.setenv("DASC_REFRESH_KERNEL", "column")
-    b = run_refresh(sh, pool, 0, lib["inv_row"], inp, 160)
+    b = run_refresh(sh, pool, 0, lib["inv_row"], inp, 160, kernel="column")
     om = lib["inv_row"] < 0
     diff = np.abs(a.reshape(n_req, -1, 128)[:, om] - b.reshape(n_req, -1, 128)[:, om]).max()
     scale = np.abs(b.reshape(n_req, -1, 128)[:, om]).max()
@@ -222,7 +227,7 @@ def test_chunked_and_column_kernels_agree(monkeypatch):
     assert np.array_equal(a.reshape(n_req, -1, 128)[:, ~om], b.reshape(n_req, -1, 128)[:, ~om])
 
 
-def test_gdn_scalar_gate_kernel_matches_channel_kernel(monkeypatch):
+def test_gdn_scalar_gate_kernel_matches_channel_kernel():
     # GDN heads take the scalar-gate kernel; the channel-wise kernel must give the same
     # state to within both kernels' distance from the oracle, and both stay in the bar
     wl = WORKLOADS["qwen_gdn"]
@@ -232,8 +237,7 @@ def test_gdn_scalar_gate_kernel_matches_channel_kernel(monkeypatch):
     pool = restored_states(wl, lib, n_req)
     inp = refresh_inputs(wl, W, log_lambda(wl)[layer], n_req=n_req, salt=layer)
     a = run_refresh(sh, pool, layer, lib["inv_row"], inp, W)
-    monkeypatch.setenv("DASC_REFRESH_KERNEL", "wy")
-    b = run_refresh(sh, pool, layer, lib["inv_row"], inp, W)
+    b = run_refresh(sh, pool, layer, lib["inv_row"], inp, W, kernel="channel_wy")
     lo = layer * sh.n_heads * sh.dk
     om = (lib["inv_row"][lo:lo + sh.n_heads * sh.dk] < 0).reshape(sh.n_heads, sh.dk)
     pairs = sample_pairs(n_req, sh.n_heads, om, 6, seed=1)

@@ -127,8 +127,11 @@ def test_padded_layout_matches_ragged_and_round_trips(arch, w):
     L, H, dk, dv, n = 4, 3, 8, 4, 3
     p = _plan(arch, L, H, dk, dv, w, seed=5)
     rpu = p["rows_per_unit"]
-    r_layer = np.diff(p["layer_off"])
-    r_max_rows = int(r_layer.max()) * rpu
+    # the plan's padded geometry against a brute-force count of kept dense rows per layer
+    kept_rows = (p["inv_row"].reshape(L, -1) >= 0).sum(axis=1)
+    assert p["r_max_rows"] == kept_rows.max()
+    np.testing.assert_array_equal(p["layer_off_rows"], np.concatenate([[0], np.cumsum(kept_rows)]))
+    r_max_rows = int(p["r_max_rows"])
     st = _words(rng, n, L * H * dk, dv)
     sentinel = np.uint32(0xDEADBEEF)
     ckpt = np.full((L, n + 1, r_max_rows, dv), sentinel, np.uint32)

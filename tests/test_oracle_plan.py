@@ -186,6 +186,44 @@ def test_compression_ratios_closed_form():
     assert p["c_ckpt"] == (8 * ub + 10) / (4 * ub + 10)
 
 
+# Sec. 4.3 / Eq. 6 / Eq. 8 at T > 1, worked by hand.  One KDA layer, H = 2 heads of
+# dk = 5 channels, dv = 4 (a unit is 4 fp32 = 16 B), T = 4 ranks, 8 conv bytes per rank.
+# Head 0 keeps channels {0, 1, 2, 4}, head 1 keeps {1, 3, 4}: 7 of 10 units retained.
+#   C = ceil(7 / 4) = 2 units per rank slice; rank_begin = [0, 2, 4, 6, 7].
+#   Owners: head h is computed on rank floor(h * 4 / 2) = 2h, so packed units 0..3 (head 0)
+#   belong to rank 0 and 4..6 (head 1) to rank 2; unit p is stored on rank floor(p / 2):
+#   send[0][0] = 2, send[0][1] = 2, send[2][2] = 2, send[2][3] = 1.
+#   Dense per-rank bytes: ceil(10 / 4) = 3 units = 48 B, + 8 conv = 56.
+#   Ragged per-rank bytes (the bottleneck after balancing): C = 2 units = 32 B, + 8 = 40.
+#   C_ckpt = 56 / 40 = 1.4; Eq. 8 with a 4000 B budget: floor(4000 / 40) - 1 = 99 slots.
+# Rounding either quotient down instead (floor for ceil) gives C = 1 and 2 dense units:
+# slot bytes 24 and 40, C_ckpt 40 / 24 = 1.67 (or 2.33 / 1.0 when only one is floored),
+# 165 slots -- every figure below would fail.
+HAND_T4 = {"C": 2, "rank_begin": [0, 2, 4, 6, 7], "slot_bytes_rank": 40,
+           "dense_slot_bytes_rank": 56, "c_ckpt": 1.4, "slots_4000": 99,
+           "send": [[2, 2, 0, 0], [0, 0, 0, 0], [0, 0, 2, 1], [0, 0, 0, 0]]}
+
+
+def hand_t4_decay():
+    """Static log-decay of the hand-worked T = 4 case (kept: H_s = 1000, omitted: H_s = 2,
+    against W_max = 16)."""
+    keep = np.array([[[1, 1, 1, 0, 1], [0, 1, 0, 1, 1]]], dtype=bool)
+    return np.where(keep, math.log(1e-3) / 1000.0, math.log(1e-3) / 2.0)
+
+
+def test_rank_bottleneck_hand_worked_t4():
+    p = P.build_plan(hand_t4_decay(), "kda", 1, 2, 5, 4, w_max=16, n_ranks=4, conv_bytes=8)
+    assert p["n_units"] == 7
+    assert p["slice_units"] == HAND_T4["C"] and p["slice_rows"] == HAND_T4["C"]
+    np.testing.assert_array_equal(p["rank_begin"], HAND_T4["rank_begin"])
+    np.testing.assert_array_equal(p["send"], HAND_T4["send"])
+    assert p["slot_bytes_rank"] == HAND_T4["slot_bytes_rank"]
+    assert p["dense_slot_bytes_rank"] == HAND_T4["dense_slot_bytes_rank"]
+    assert p["c_ckpt"] == HAND_T4["c_ckpt"]
+    assert p["c_temp_rag"] == 10 / 7
+    assert P.matched_slots(4000, p["slot_bytes_rank"]) == HAND_T4["slots_4000"]
+
+
 def test_matched_hbm_slots_golden():
     gold = json.load(open(os.path.join(GOLD, "matched_hbm.json")))
     for arch in ("kda", "gdn"):

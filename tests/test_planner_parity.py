@@ -19,10 +19,11 @@ def _compare(sh, a_log, mode, k, w, T=1, conv=0, eps=1e-3):
     orc = OP.build_plan(g_orc, sh.arch, sh.n_layers, sh.n_heads, sh.dk, sh.dv, w, mode, k, eps, T, conv)
     assert lib["horizon"].tobytes() == orc["horizon"].tobytes()
     np.testing.assert_array_equal(lib["keep"], orc["keep"])
-    for name in ("unit_count", "off", "layer_off", "unit_row", "inv_row", "w_units", "rank_begin", "send"):
+    for name in ("unit_count", "off", "layer_off", "layer_off_rows", "unit_row", "inv_row", "w_units",
+                 "rank_begin", "send"):
         np.testing.assert_array_equal(lib[name], orc[name], err_msg=name)
     for name in ("n_rows", "n_units", "rows_per_unit", "w_replay", "slice_units", "slice_rows",
-                 "slot_bytes_rank", "dense_slot_bytes_rank"):
+                 "r_max_rows", "slot_bytes_rank", "dense_slot_bytes_rank"):
         assert lib[name] == orc[name], name
     for name in ("c_temp_rag", "c_temp_pad", "layout_gain", "c_ckpt"):
         a, b = lib[name], orc[name]
@@ -116,3 +117,18 @@ def test_random_tp_permutation_bit_exact(arch, L, B, g, T, dk, seed, ties):
         uc = np.minimum(uc, hi)
     sh = D.Shape(arch, L, H, B, dk, 4)
     _compare_perm(sh, uc, T)
+
+
+def test_rank_bottleneck_hand_worked_t4_library():
+    # the hand-worked T = 4 case of the oracle pins, through the C ABI
+    from tests.test_oracle_plan import HAND_T4, hand_t4_decay
+
+    sh = D.Shape("kda", 1, 2, 2, 5, 4)
+    p = D.dasc_plan(sh, hand_t4_decay(), "threshold", 0, 16, 4, 1e-3, 8)
+    assert p["n_units"] == 7 and p["slice_units"] == HAND_T4["C"]
+    np.testing.assert_array_equal(p["rank_begin"], HAND_T4["rank_begin"])
+    np.testing.assert_array_equal(p["send"], HAND_T4["send"])
+    assert p["slot_bytes_rank"] == HAND_T4["slot_bytes_rank"]
+    assert p["dense_slot_bytes_rank"] == HAND_T4["dense_slot_bytes_rank"]
+    assert p["c_ckpt"] == HAND_T4["c_ckpt"]
+    assert D.dasc_matched_slots(4000, p["slot_bytes_rank"]) == HAND_T4["slots_4000"]
