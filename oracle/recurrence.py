@@ -167,3 +167,23 @@ def refresh_error(got: np.ndarray, want: np.ndarray, omitted: np.ndarray, pairs:
         err = np.abs(np.asarray(got[i], dtype=np.float64)[m] - want[i][m]).max()
         worst = max(worst, err / ref if ref > 0 else err)
     return worst
+
+
+def refresh_error_elementwise(got: np.ndarray, want: np.ndarray, omitted: np.ndarray,
+                              pairs: list, floor: float = 1e-3) -> float:
+    """Largest element-wise relative error over refreshed rows, with an absolute floor:
+    max |got - want| / max(|want|, floor * max |want|), the floor taken per (request,
+    head) so that entries near zero do not divide by ~0.
+
+    got, want: [len(pairs), dk, dv]; omitted: [H, dk]."""
+    worst = 0.0
+    for i, (_, h) in enumerate(pairs):
+        m = omitted[h]
+        if not m.any():
+            continue
+        w = want[i][m]
+        den = np.maximum(np.abs(w), floor * np.abs(w).max())
+        den = np.where(den > 0, den, 1.0)
+        err = np.abs(np.asarray(got[i], dtype=np.float64)[m] - w) / den
+        worst = max(worst, float(err.max()))
+    return worst

@@ -2,6 +2,7 @@
 
 from __future__ import annotations
 
+import functools
 import sys
 
 import numpy as np
@@ -52,3 +53,41 @@ def dev_bf16(bits: np.ndarray):
 def host_words(t) -> np.ndarray:
     """Device fp32 tensor -> host uint32 words (bit-exact)."""
     return t.cpu().numpy().view(np.uint32)
+
+
+def restored_states(wl: Workload, plan, n_req: int, salt: int = 0) -> np.ndarray:
+    """Restored active states [n_req, L, H, dk, dv] fp32: states_host packed and restored
+    on the host by the oracle (retained rows kept, omitted rows +0.0)."""
+    from oracle import pack as OK
+    from workloads import states_host
+
+    st = states_host(wl, n_req, salt=salt)
+    words = st.reshape(n_req, -1, wl.dv).view(np.uint32)
+    R = int(plan["n_rows"])
+    ck = OK.pack(words, list(range(n_req)), plan["unit_row"],
+                 np.zeros((1, n_req, R, wl.dv), np.uint32), list(range(n_req)))
+    back = OK.restore(ck, list(range(n_req)), plan["unit_row"], np.zeros_like(words),
+                      list(range(n_req)))
+    full = back.view(np.float32).reshape(n_req, wl.n_layers, wl.n_heads, wl.dk, wl.dv)
+    return np.ascontiguousarray(full)
+
+
+@functools.lru_cache(maxsize=2)
+def kimi_layer_oracle(W: int):
+    """The serving-shape KDA layer (16 requests x 32 heads, 128 x 128) at window W: the
+    plan, the restored pool, the suffix inputs and the fp64 oracle refresh of EVERY
+    refreshed (request, head).  Computed once per window and shared by the refresh and
+    fused-load tests (request i restores from source state i in both)."""
+    from oracle import recurrence as OR
+    from workloads import WORKLOADS, refresh_inputs
+
+    wl = WORKLOADS["kimi_layer"]
+    lib, _ = plans(wl)
+    pool = restored_states(wl, lib, wl.n_req)
+    inp = refresh_inputs(wl, W, log_lambda(wl)[0])
+    om = (lib["inv_row"] < 0).reshape(wl.n_heads, wl.dk)
+    pairs = [(n, h) for n in range(wl.n_req) for h in range(wl.n_heads) if om[h].any()]
+    announce(f"fp64 oracle: {len(pairs)} (request, head) pairs at W={W}")
+    want, om2 = OR.refresh(pool[:, 0], lib["inv_row"], inp["k"], inp["v"], inp["g"], inp["beta"],
+                           wl.n_qk_heads, "restored", pairs=pairs)
+    return wl, lib, pool, inp, pairs, want, om2

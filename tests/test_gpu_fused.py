@@ -13,7 +13,7 @@ import pytest
 import paper_2608_30386_amd as D
 from oracle import pack as OK
 from oracle import recurrence as OR
-from tests.gpu_util import announce, dev, dev_bf16, dev_i32, plans, shape_of
+from tests.gpu_util import announce, dev, dev_bf16, dev_i32, kimi_layer_oracle, plans, shape_of
 from tests.test_gpu_refresh import _inputs_128, sample_pairs
 from workloads import WORKLOADS, log_lambda, refresh_inputs, states_host
 
@@ -65,19 +65,26 @@ def run_unfused(sh, layer, ck, ck_slots, inv_row, pool, dst, inp, W, n_rows, n_r
     return states.cpu().numpy()
 
 
-def check_fused(sh, layer, got, restored, inv_row, dst, inp, pairs, init, n_pool):
-    """Refreshed rows vs the oracle on `pairs`; the layer's other rows are the restored
-    rows bit for bit; other layers and other pool slots keep the sentinel."""
+def check_fused(sh, layer, got, restored, inv_row, dst, inp, pairs, init, n_pool, oracle=None,
+                report=None):
+    """Refreshed rows vs the oracle on `pairs` (computed here, or given as `oracle` =
+    (want, omitted)); the layer's other rows are the restored rows bit for bit; other
+    layers and other pool slots keep the sentinel."""
     H, dk, dv = sh.n_heads, sh.dk, sh.dv
     n_req = len(dst)
     lo, hi = layer * H * dk, (layer + 1) * H * dk
     inv_layer = inv_row[lo:hi]
-    layer_in = restored.view(np.float32)[:, lo:hi].reshape(n_req, H, dk, dv)
-    want, om = OR.refresh(layer_in, inv_layer, inp["k"], inp["v"], inp["g"], inp["beta"],
-                          sh.n_qk_heads, init, pairs=pairs)
+    if oracle is None:
+        layer_in = restored.view(np.float32)[:, lo:hi].reshape(n_req, H, dk, dv)
+        want, om = OR.refresh(layer_in, inv_layer, inp["k"], inp["v"], inp["g"], inp["beta"],
+                              sh.n_qk_heads, init, pairs=pairs)
+    else:
+        want, om = oracle
     g4 = got.reshape(n_pool, -1, dk, dv)
     g_pairs = np.stack([g4[dst[n], layer * H + h] for n, h in pairs])
     err = OR.refresh_error(g_pairs, want, om, pairs)
+    if report is not None:
+        report["elementwise"] = OR.refresh_error_elementwise(g_pairs, want, om, pairs)
     assert err <= TOL, f"refresh error {err:.3e} > {TOL}"
     words = got.reshape(n_pool, -1, dv).view(np.uint32)
     keep = ~om.reshape(-1)                              # rows of the layer not refreshed
@@ -109,15 +116,25 @@ def test_kimi_layer_fused(W):
     n_pool = n_req + 2
     dst = [(5 * i + 1) % n_pool for i in range(n_req)]   # distinct: gcd(5, 18) = 1
     pool = sentinel_pool(n_pool, sh)
-    inp = refresh_inputs(wl, W, log_lambda(wl)[0])
-    got = run_fused(sh, 0, ck, ck_slots, lib["inv_row"], pool, dst, inp, W, R, 1, R)
     om = (lib["inv_row"] < 0).reshape(wl.n_heads, wl.dk)
-    pairs = sample_pairs(n_req, wl.n_heads, om, 8, seed=W)
-    err = check_fused(sh, 0, got, restored, lib["inv_row"], dst, inp, pairs, "restored", n_pool)
+    rep, oracle = {}, None
+    if W == 1024:
+        # the serving shape's oracle over every refreshed head (request i restores from
+        # source state i here as in the refresh test, with the same suffix inputs)
+        _, _, pool_o, inp, pairs, want, om_o = kimi_layer_oracle(W)
+        np.testing.assert_array_equal(pool_o.reshape(n_req, -1, wl.dv).view(np.uint32), restored)
+        oracle = (want, om_o)
+    else:
+        inp = refresh_inputs(wl, W, log_lambda(wl)[0])
+        pairs = sample_pairs(n_req, wl.n_heads, om, 8, seed=W)
+    got = run_fused(sh, 0, ck, ck_slots, lib["inv_row"], pool, dst, inp, W, R, 1, R)
+    err = check_fused(sh, 0, got, restored, lib["inv_row"], dst, inp, pairs, "restored", n_pool,
+                      oracle=oracle, report=rep)
     ref = run_unfused(sh, 0, ck, ck_slots, lib["inv_row"], pool, dst, inp, W, R, 1, R)
     g, r = got.reshape(n_pool, -1).view(np.uint32), ref.reshape(n_pool, -1).view(np.uint32)
     assert np.array_equal(g[dst], r[dst]), "fused differs from restore + refresh"
-    announce(f"kimi_layer fused W={W} sampled max rel err {err:.2e}, bit-equal to unfused")
+    announce(f"kimi_layer fused W={W}: {len(pairs)} heads vs oracle, max per-head rel err "
+             f"{err:.2e}, element-wise {rep['elementwise']:.2e}; bit-equal to unfused")
 
 
 @pytest.mark.parametrize("arch,init", [("kda", "restored"), ("kda", "zero"), ("gdn", "restored"),
@@ -168,11 +185,12 @@ def test_qwen_gdn_fused_one_layer():
     got = run_fused(sh, layer, ck, ck_slots, lib["inv_row"], pool, dst, inp, 1024, R, 1, R)
     lo = layer * sh.n_heads * sh.dk
     om = (lib["inv_row"][lo:lo + sh.n_heads * sh.dk] < 0).reshape(sh.n_heads, sh.dk)
-    pairs = sample_pairs(n_req, sh.n_heads, om, 6, seed=layer)
+    pairs = [(n, h) for n in range(n_req) for h in range(sh.n_heads) if om[h].any()]   # all 80
     err = check_fused(sh, layer, got, restored, lib["inv_row"], dst, inp, pairs, "restored", n_pool)
     ref = run_unfused(sh, layer, ck, ck_slots, lib["inv_row"], pool, dst, inp, 1024, R, 1, R)
     hi = lo + sh.n_heads * sh.dk
     g_ = got.reshape(n_pool, -1, sh.dv).view(np.uint32)[:, lo:hi]
     r_ = ref.reshape(n_pool, -1, sh.dv).view(np.uint32)[:, lo:hi]
     assert np.array_equal(g_[dst], r_[dst]), "fused differs from restore + refresh"
-    announce(f"qwen_gdn fused layer={layer} sampled max rel err {err:.2e}, bit-equal to unfused")
+    announce(f"qwen_gdn fused layer={layer}: all {len(pairs)} heads, max rel err {err:.2e}, "
+             "bit-equal to unfused")
