@@ -25,7 +25,8 @@
  *   - Every argument the host can see is validated before any launch; a failed
  *     check returns an error and launches nothing.
  *   - The caller owns all memory.  The library allocates no device memory and
- *     keeps no state between calls.
+ *     keeps no state between calls, except the static device scratch array of
+ *     dasc_refresh_noalloc (see there).
  *   - Device calls are asynchronous on the given stream and never synchronise.
  *     A NULL stream means the default (null) stream.
  *   - Indices that live in device memory (slot lists, row maps) cannot be seen
@@ -57,6 +58,7 @@ extern "C" {
  * earlier error of the caller's matters.  Errors that happen while a kernel runs surface
  * at the caller's next synchronisation, as for any asynchronous launch. */
 #define DASC_E_UNSUPPORTED -5  /* valid request with no kernel built for it      */
+#define DASC_E_SCRATCH     -6  /* needs more than the static scratch of dasc_refresh_noalloc */
 
 /* Longest replay window dasc_refresh accepts (tokens): keeps every per-head input
  * stream of a dk = 128 head within 1 GiB. */
@@ -325,6 +327,33 @@ int dasc_refresh(const dasc_shape *shape, int32_t layer, const int32_t *inv_row,
                  const uint16_t *k, const uint16_t *v, const float *g, const float *beta,
                  int32_t n_req, int32_t W, int32_t init_mode,
                  void *workspace, size_t workspace_bytes, dasc_stream_t stream);
+
+/* ---- Load with refresh, allocating nothing -------------------------------- */
+
+/* Size of the device scratch array dasc_refresh_noalloc uses in place of a workspace
+ * (64 MiB per device: the GDN factor records of, for example, 16 requests x 32 heads at
+ * W = 1024, or 8 requests x 32 heads at W = 2048). */
+#define DASC_NOALLOC_SCRATCH_BYTES (64ll << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): dasc_refresh with no workspace
+ * argument.  The scratch dasc_refresh would take from the workspace (the GDN factor
+ * records, dasc_refresh_workspace_bytes of them) lives in a device array inside the
+ * library, DASC_NOALLOC_SCRATCH_BYTES on each device it runs on, held until the process
+ * ends; its device address is looked up once per device, on the first call with that
+ * device current.  The call allocates nothing (no hipMalloc, no allocating library
+ * routine).  Arguments, layouts, results and precision are those of dasc_refresh; the
+ * kernels are the same, so the results are bit-identical to dasc_refresh's.
+ * Every call on one device shares that device's array: calls that overlap on one device
+ * (different streams, or threads without ordering) race and must not be issued.  The
+ * stream must belong to the current device.
+ * Errors: those of dasc_refresh (without DASC_E_WORKSPACE); DASC_E_SCRATCH, before
+ * anything is launched, when dasc_refresh_workspace_bytes for this shape, n_req and W
+ * exceeds DASC_NOALLOC_SCRATCH_BYTES; DASC_E_HIP if the array's address cannot be found. */
+int dasc_refresh_noalloc(const dasc_shape *shape, int32_t layer, const int32_t *inv_row,
+                         float *states, int64_t n_pool, const int32_t *slot,
+                         const uint16_t *k, const uint16_t *v, const float *g, const float *beta,
+                         int32_t n_req, int32_t W, int32_t init_mode, dasc_stream_t stream);
 
 /* ---- Load with refresh, fused (Sec. 4.2: restore, then DASC-WR) ----------- */
 

@@ -15,6 +15,7 @@ from .dasc import (  # noqa: F401
     dasc_pack_q8,
     dasc_plan,
     dasc_refresh,
+    dasc_refresh_noalloc,
     dasc_refresh_select,
     dasc_refresh_workspace_bytes,
     dasc_restore,

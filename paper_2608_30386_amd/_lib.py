@@ -17,6 +17,8 @@ DASC_E_SHAPE = -2
 DASC_E_WORKSPACE = -3
 DASC_E_HIP = -4
 DASC_E_UNSUPPORTED = -5
+DASC_E_SCRATCH = -6
+DASC_NOALLOC_SCRATCH_BYTES = 64 << 20
 DASC_MAX_WINDOW = 1 << 21
 
 DASC_ARCH_KDA = 0
@@ -35,6 +37,7 @@ EXPORTED = (
     "dasc_pack", "dasc_restore", "dasc_pack_q8", "dasc_restore_q8",
     "dasc_refresh_workspace_bytes", "dasc_refresh", "dasc_restore_refresh",
     "dasc_tp_permutation", "dasc_pack_padded", "dasc_restore_padded", "dasc_refresh_select",
+    "dasc_refresh_noalloc",
 )
 
 
@@ -103,6 +106,7 @@ def _load() -> C.CDLL:
         "dasc_restore_q8": [C.POINTER(Shape), P, P, I64, P, I64, P, P, I64, P, I32, P],
         "dasc_refresh_workspace_bytes": [C.POINTER(Shape), I32, I32, C.POINTER(C.c_size_t)],
         "dasc_refresh": [C.POINTER(Shape), I32, P, P, I64, P, P, P, P, P, I32, I32, I32, P, SZ, P],
+        "dasc_refresh_noalloc": [C.POINTER(Shape), I32, P, P, I64, P, P, P, P, P, I32, I32, I32, P],
         "dasc_refresh_select": [C.POINTER(Shape), I32, P, P, I64, P, P, P, P, P, I32, I32, I32, P, SZ,
                                 I32, P],
         "dasc_restore_refresh": [C.POINTER(Shape), I32, P, I64, P, I32, I64, I64, P, P, I64, P,

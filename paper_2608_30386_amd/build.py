@@ -24,7 +24,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdasc.so")
 
-HIP_SOURCES = ["pack_restore.hip", "quant.hip", "refresh.hip", "refresh_wy.hip", "refresh_wy_gdn.hip"]
+HIP_SOURCES = ["pack_restore.hip", "quant.hip", "refresh.hip", "refresh_wy.hip", "refresh_wy_gdn.hip",
+               "refresh_noalloc.hip"]
 HOST_SOURCES = ["plan.cpp"]
 ARCH = "gfx950"
 

@@ -295,6 +295,9 @@ extern "C" const char* dasc_strerror(int code) {
     case DASC_E_WORKSPACE: return "workspace too small";
     case DASC_E_HIP: return "HIP runtime error at launch";
     case DASC_E_UNSUPPORTED: return "no kernel built for this shape";
+    case DASC_E_SCRATCH:
+      return "request needs more scratch than dasc_refresh_noalloc holds "
+             "(DASC_NOALLOC_SCRATCH_BYTES); use dasc_refresh with a workspace";
     default: return "unknown status code";
   }
 }

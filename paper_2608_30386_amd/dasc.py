@@ -330,6 +330,15 @@ def dasc_refresh(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta,
     del ws
 
 
+def dasc_refresh_noalloc(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta, W: int,
+                         init_mode: str = "restored", stream=None) -> None:
+    """dasc_refresh without a workspace: the library's static device scratch stands in for
+    it (dasc.h), so neither this call nor the library allocates device memory."""
+    a = _refresh_args(shape, inv_row, states, slot, k, v, g, beta, W)
+    _check(LIB.dasc_refresh_noalloc(C.byref(shape.c()), layer, *a, W, INIT[init_mode],
+                                    _stream(stream)), "dasc_refresh_noalloc")
+
+
 def dasc_refresh_select(shape: Shape, layer: int, inv_row, states, slot, k, v, g, beta, W: int,
                         kernel: str, init_mode: str = "restored", workspace=None,
                         stream=None) -> None:

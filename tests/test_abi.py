@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 16
     assert set(names) == set(_lib.EXPORTED)
     lib = C.CDLL(_lib.LIB_PATH)
     for n in names:
@@ -127,7 +127,7 @@ def test_padded_argument_errors():
 
 
 def test_strerror_total():
-    for code in (0, -1, -2, -3, -4, -5, 7, -99):
+    for code in (0, -1, -2, -3, -4, -5, -6, 7, -99):
         assert LIB.dasc_strerror(code)
 
 
@@ -232,6 +232,36 @@ def test_refresh_select_argument_errors():
     for src in ("refresh.hip", "refresh_wy.hip", "refresh_wy_gdn.hip"):
         text = open(os.path.join(ROOT, "paper_2608_30386_amd", "csrc", src)).read()
         assert "getenv" not in text, src
+
+
+def test_refresh_noalloc_argument_errors():
+    # host-side checks of the entry point that allocates nothing: arguments are those of
+    # dasc_refresh, and a request whose factor records exceed the static scratch is
+    # refused before anything touches the device
+    E = _lib
+
+    def na(shape, n_req=1, W=8, ptrs=None):
+        p = dict(inv=FAKE, states=FAKE, slot=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE)
+        p.update(ptrs or {})
+        return LIB.dasc_refresh_noalloc(C.byref(shape) if shape is not None else None, 0,
+                                        p["inv"], p["states"], 1, p["slot"], p["k"], p["v"],
+                                        p["g"], p["beta"], n_req, W, 0, None)
+
+    assert na(None) == E.DASC_E_INVAL
+    assert na(kda(), W=0) == E.DASC_E_INVAL
+    assert na(kda(), n_req=0) == E.DASC_E_INVAL
+    assert na(kda(dv=6)) == E.DASC_E_SHAPE
+    for name in ("inv", "states", "slot", "k", "v", "g", "beta"):
+        assert na(kda(), ptrs={name: None}) == E.DASC_E_INVAL, name
+    gdn = Shape(_lib.DASC_ARCH_GDN, 1, 32, 16, 128, 128)
+    need = C.c_size_t(0)
+    assert LIB.dasc_refresh_workspace_bytes(C.byref(gdn), 3, 8192, C.byref(need)) == E.DASC_OK
+    assert need.value > E.DASC_NOALLOC_SCRATCH_BYTES
+    assert na(gdn, n_req=3, W=8192) == E.DASC_E_SCRATCH
+    assert b"scratch" in LIB.dasc_strerror(E.DASC_E_SCRATCH)
+    # the largest request that fits: 16 requests x 32 heads x 32 chunks x 4 KiB = 64 MiB
+    assert LIB.dasc_refresh_workspace_bytes(C.byref(gdn), 16, 1024, C.byref(need)) == E.DASC_OK
+    assert need.value == E.DASC_NOALLOC_SCRATCH_BYTES
 
 
 def test_plan_padded_geometry_fields():
