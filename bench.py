@@ -12,7 +12,20 @@ offline); its host time is reported separately.
 
 Prints one JSON line.  `value` is suffix tokens refreshed per second of whole-step
 time (n_req * W / step time); per-kernel rates are in `kernels`.  All inputs are
-resident in HBM before the timed region starts.
+resident in HBM before any timed region starts.
+
+Order of work on the GPU:
+  1. per-kernel durations of the step's kernels, from HIP events around batches of
+     back-to-back launches of one kernel (median over batches);
+  2. the other configurations, as extra keys: the full-model KDA checkpoint set (24
+     layers, 256 checkpoints, T = 8 rank slices) pack/restore, and the Qwen-GDN refresh
+     of 8 requests x 36 layers (`extra`);
+  3. the headline: --warmup untimed steps, then exactly --steps timed steps between
+     two synchronisations.  From an idle GPU the clock takes ~25 back-to-back steps to
+     settle under this load; by the time step 3 runs, steps 1-2 have kept the GPU busy
+     for several seconds.  `first_pass_ms_per_step` is the same measurement taken as
+     the very first GPU work of the process (cold clock), for comparison;
+  4. the CPU baseline (the oracle on the host cores, at 1 thread and at all of them).
 
     python bench.py [--steps K] [--warmup W] [--workload kimi_headline|kimi_model|qwen_gdn]
 """
@@ -38,20 +51,20 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # dense bf16 matrix peak
 # and K_H^T U (128*32*128), per 32 tokens, 2 FLOP per MAC.
 WY_FLOP_PER_HEAD_TOKEN = 2.0 * (3 * 16 * 16 * 128 + 32 * 128 * 128 + 32 * 32 * 128 + 128 * 32 * 128) / 32
 METRIC = "pack/restore GB/s + suffix-refresh tokens/s (KDA 32h x 128x128, W=1024)"
+MAX_POOL_THREADS = 16           # the host CPU share of one GPU on the benchmark machines
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    # From idle, the clock takes about 25 back-to-back steps to settle under this load: the
-    # refresh launch time climbs from 295 to 350 us and comes back to 300 us over the
-    # first 23 launches of a run, then stays at 280-300 us.
     ap.add_argument("--warmup", type=int, default=25)
     ap.add_argument("--workload", default="kimi_headline",
                     choices=["kimi_headline", "kimi_model", "qwen_gdn"])
     ap.add_argument("--W", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="headline only: skip the full-model KDA and Qwen-GDN extra keys")
     ap.add_argument("--no-other-windows", action="store_true",
                     help="time the refresh at the headline window only (counter runs average "
                          "every dispatch of a kernel, so the other windows would mix in)")
@@ -67,7 +80,8 @@ def kernel_source_hash() -> str:
     and the build script with its compiler flags."""
     h = hashlib.sha256()
     for f in ("pack_restore.hip", "quant.hip", "refresh.hip", "refresh_wy.hip", "refresh_wy_gdn.hip",
-              "ckpt_layout.h", "refresh_kernels.h", "launch_common.h", "wy_ops.h"):
+              "refresh_noalloc.hip", "ckpt_layout.h", "refresh_kernels.h", "launch_common.h",
+              "wy_ops.h"):
         with open(os.path.join(ROOT, "paper_2608_30386_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     with open(os.path.join(ROOT, "paper_2608_30386_amd", "build.py"), "rb") as fh:
@@ -95,23 +109,23 @@ def measured_util(key: str, what: str):
     return _counter_summary().get("utilisation", {}).get(key, {}).get(what)
 
 
-class KernelTimer:
-    """HIP events around launches on the stream the library is given."""
-
-    def __init__(self, torch):
-        self.torch = torch
-        self.spans = {}
-
-    def run(self, name, fn):
-        ev0 = self.torch.cuda.Event(enable_timing=True)
-        ev1 = self.torch.cuda.Event(enable_timing=True)
-        ev0.record()
+def batched_ms(torch, fn, batches: int = 10, per_batch: int = 10, warm: int = 3) -> float:
+    """Duration of one call of `fn` on the GPU (ms): HIP events on torch's current stream
+    (the stream the library launches on) around `batches` runs of `per_batch`
+    back-to-back calls, the median over the batches of elapsed / per_batch.  Events around
+    whole batches add no per-launch gap."""
+    for _ in range(warm):
         fn()
-        ev1.record()
-        self.spans.setdefault(name, []).append((ev0, ev1))
-
-    def mean_ms(self, name):
-        return float(np.mean([a.elapsed_time(b) for a, b in self.spans[name]]))
+    spans = []
+    for _ in range(batches):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(per_batch):
+            fn()
+        e1.record()
+        spans.append((e0, e1))
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) / per_batch for a, b in spans]))
 
 
 def copy_calibration(torch):
@@ -131,18 +145,9 @@ def copy_bandwidth(torch, args):
     n = 1 << 30
     src = torch.ones(n, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
-    for _ in range(args.warmup):
-        dst.copy_(src)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        dst.copy_(src)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = batched_ms(torch, lambda: dst.copy_(src), batches=5, per_batch=max(args.steps // 5, 1))
     print(json.dumps({"copy_bytes": 2 * n * 4, "ms": ms, "GBps": 2 * n * 4 / ms / 1e6,
-                      "steps": args.steps, "warmup": args.warmup}))
+                      "steps": args.steps}))
 
 
 def main():
@@ -165,7 +170,7 @@ def main():
     if args.workload == "kimi_headline":
         out = bench_headline(torch, args)
     elif args.workload == "kimi_model":
-        out = bench_pack_restore_only(torch, args, "kimi_model")
+        out = bench_full_model(torch, args)
     else:
         out = bench_gdn(torch, args)
     print(json.dumps(out))
@@ -174,8 +179,8 @@ def main():
 # ---------------------------------------------------------------------------------------
 
 def timed_steps(torch, fn, args) -> float:
-    """Warm up, then wall-clock exactly args.steps calls between two synchronisations (ms
-    per call)."""
+    """args.warmup untimed calls, then wall-clock exactly args.steps calls between two
+    synchronisations (ms per call)."""
     for _ in range(args.warmup):
         fn()
     torch.cuda.synchronize()
@@ -205,6 +210,20 @@ def _bf16(torch, bits):
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
 
 
+def _rate(ms, nbytes):
+    return {"ms": ms, "GBps": nbytes / ms / 1e6, "hbm_frac": nbytes / ms / 1e6 / HBM_PEAK_GBPS,
+            "bytes": nbytes}
+
+
+def kda_refresh_bytes(sh, plan, n_req, W):
+    """Algorithmic bytes of one KDA refresh launch: per refreshed head k, v (bf16), g,
+    beta (fp32) and the restored state read; the omitted rows written."""
+    omitted = (plan["inv_row"] < 0).reshape(sh.n_heads, sh.dk)
+    heads = int(omitted.any(axis=1).sum())
+    per_head = 2 * W * sh.dk + 2 * W * sh.dv + 4 * W * sh.dk + 4 * W + 4 * sh.dk * sh.dv
+    return per_head, heads, n_req * (heads * per_head + int(omitted.sum()) * sh.dv * 4)
+
+
 def bench_headline(torch, args):
     import paper_2608_30386_amd as D
     from workloads import WORKLOADS, log_lambda, refresh_inputs, states_host
@@ -228,61 +247,38 @@ def bench_headline(torch, args):
     g, beta = torch.from_numpy(inp["g"]).cuda(), torch.from_numpy(inp["beta"]).cuda()
     torch.cuda.synchronize()
 
-    timer = KernelTimer(torch)
-
-    def plain_step():
+    def pack():
         D.dasc_pack(sh, states, ids, unit_row, ckpt, ids)
+
+    def restore():
         D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R)
+
+    def refresh():
         D.dasc_refresh(sh, 0, inv_row, active, req, k, v, g, beta, W)
 
     def step():
-        timer.run("pack", lambda: D.dasc_pack(sh, states, ids, unit_row, ckpt, ids))
-        timer.run("restore", lambda: D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R))
-        timer.run("refresh", lambda: D.dasc_refresh(sh, 0, inv_row, active, req, k, v, g, beta, W))
+        pack()
+        restore()
+        refresh()
 
-    # the timed steps are plain launches; events around each launch add about 10 us of
-    # GPU-side gap per kernel, so the per-kernel durations come from a second pass.
-    # (A HIP graph of the three launches replays slower here: 0.405 vs 0.357 ms.)
-    ms_step = timed_steps(torch, plain_step, args)
+    # the headline measurement as the first GPU work of the process (cold clock)
+    first_ms = timed_steps(torch, step, args)
 
-    # per-kernel durations: HIP events around each launch, on the library's stream
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    timer.spans.clear()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-
+    # 1. per-kernel durations
+    t = {"pack": batched_ms(torch, pack), "restore": batched_ms(torch, restore),
+         "refresh": batched_ms(torch, refresh)}
     # Load with refresh of the refreshed requests: dasc_restore + dasc_refresh (two launches)
-    # against the fused dasc_restore_refresh (one launch, the same result bit for bit)
-    def load_wr():
-        timer.run("restore_req", lambda: D.dasc_restore(sh, ckpt, req, inv_row, active, req, n_rows=R))
-        timer.run("refresh_req", lambda: D.dasc_refresh(sh, 0, inv_row, active, req, k, v, g, beta, W))
-        timer.run("restore_refresh", lambda: D.dasc_restore_refresh(
-            sh, 0, ckpt, req, inv_row, active, req, k, v, g, beta, W, n_rows=R))
+    # against the fused dasc_restore_refresh (the same result bit for bit)
+    t["restore_req"] = batched_ms(torch, lambda: D.dasc_restore(sh, ckpt, req, inv_row, active, req,
+                                                                n_rows=R))
+    t["refresh_req"] = batched_ms(torch, refresh)
+    t["restore_refresh"] = batched_ms(torch, lambda: D.dasc_restore_refresh(
+        sh, 0, ckpt, req, inv_row, active, req, k, v, g, beta, W, n_rows=R))
 
-    load_wr()
-    torch.cuda.synchronize()
-    for name in ("restore_req", "refresh_req", "restore_refresh"):
-        timer.spans[name].clear()
-    for _ in range(args.steps):
-        load_wr()
-    torch.cuda.synchronize()
-
-    omitted = (plan["inv_row"] < 0).reshape(sh.n_heads, sh.dk)
-    heads_refreshed = int(omitted.any(axis=1).sum())
+    per_head, heads, bytes_refresh = kda_refresh_bytes(sh, plan, n_req, W)
     bytes_pack = 2 * R * dv * 4 * n_ckpt
     bytes_restore = (R + rows) * dv * 4 * n_ckpt
-
-    def refresh_bytes(w):
-        # refresh reads k, v, g, beta and the restored state of every refreshed head, and
-        # writes the omitted rows
-        per_head = (2 * w * sh.dk + 2 * w * dv + 4 * w * sh.dk + 4 * w + 4 * sh.dk * dv)
-        return per_head, n_req * (heads_refreshed * per_head + int(omitted.sum()) * dv * 4)
-
-    per_head, bytes_refresh = refresh_bytes(W)
-    flops_refresh = WY_FLOP_PER_HEAD_TOKEN * W * n_req * heads_refreshed
+    flops_refresh = WY_FLOP_PER_HEAD_TOKEN * W * n_req * heads
 
     # the serving shape's other replay windows (refresh alone, same requests and state)
     by_window = {}
@@ -292,43 +288,40 @@ def bench_headline(torch, args):
         inp2 = refresh_inputs(wl, w2, log_lambda(wl)[0], salt=w2)
         k2, v2 = _bf16(torch, inp2["k"]), _bf16(torch, inp2["v"])
         g2, b2 = torch.from_numpy(inp2["g"]).cuda(), torch.from_numpy(inp2["beta"]).cuda()
-        name = f"refresh_W{w2}"
-        run2 = lambda: D.dasc_refresh(sh, 0, inv_row, active, req, k2, v2, g2, b2, w2)  # noqa: E731
-        for _ in range(args.warmup):
-            run2()
-        torch.cuda.synchronize()
-        for _ in range(args.steps):
-            timer.run(name, run2)
-        torch.cuda.synchronize()
-        ms2 = timer.mean_ms(name)
-        by_window[str(w2)] = {"ms": ms2, "tokens_per_s": n_req * w2 / (ms2 / 1e3),
-                              "GBps": refresh_bytes(w2)[1] / ms2 / 1e6,
-                              "hbm_frac": refresh_bytes(w2)[1] / ms2 / 1e6 / HBM_PEAK_GBPS}
+        ms2 = batched_ms(torch, lambda: D.dasc_refresh(sh, 0, inv_row, active, req, k2, v2, g2, b2, w2))
+        b_w2 = kda_refresh_bytes(sh, plan, n_req, w2)[2]
+        by_window[str(w2)] = {"tokens_per_s": n_req * w2 / (ms2 / 1e3), **_rate(ms2, b_w2)}
         del k2, v2, g2, b2
 
-    t = {n: timer.mean_ms(n) for n in ("pack", "restore", "refresh", "restore_req", "refresh_req",
-                                       "restore_refresh")}
     # fused: suffix inputs of every refreshed head, each kept row read once, every row of
     # the layer written once
-    bytes_fused = n_req * (heads_refreshed * (per_head - 4 * sh.dk * dv) + R * dv * 4 + rows * dv * 4)
+    bytes_fused = n_req * (heads * (per_head - 4 * sh.dk * dv) + R * dv * 4 + rows * dv * 4)
     kernels = {
-        "pack": {"ms": t["pack"], "GBps": bytes_pack / t["pack"] / 1e6,
-                 "hbm_frac": bytes_pack / t["pack"] / 1e6 / HBM_PEAK_GBPS, "bytes": bytes_pack},
-        "restore": {"ms": t["restore"], "GBps": bytes_restore / t["restore"] / 1e6,
-                    "hbm_frac": bytes_restore / t["restore"] / 1e6 / HBM_PEAK_GBPS,
-                    "bytes": bytes_restore},
-        "refresh": {"ms": t["refresh"], "tokens_per_s": n_req * W / (t["refresh"] / 1e3),
-                    "GBps": bytes_refresh / t["refresh"] / 1e6,
-                    "TFLOPs": flops_refresh / t["refresh"] / 1e9, "bytes": bytes_refresh,
-                    "flops": flops_refresh, "heads": n_req * heads_refreshed},
+        "pack": _rate(t["pack"], bytes_pack),
+        "restore": _rate(t["restore"], bytes_restore),
+        "refresh": {"tokens_per_s": n_req * W / (t["refresh"] / 1e3),
+                    "TFLOPs": flops_refresh / t["refresh"] / 1e9, "flops": flops_refresh,
+                    "heads": n_req * heads, **_rate(t["refresh"], bytes_refresh)},
         "restore_refresh_fused": {
             "ms": t["restore_refresh"], "unfused_ms": t["restore_req"] + t["refresh_req"],
             "requests": n_req, "GBps": bytes_fused / t["restore_refresh"] / 1e6,
             "bytes": bytes_fused},
         "refresh_by_window": by_window,
+        "timing": "HIP events around 10 batches of 10 back-to-back launches, median",
     }
+
+    # 2. the other configurations
+    extra = {}
+    if not args.no_extra:
+        extra["kimi_model"] = full_model_keys(torch, args, layouts=("ragged",))
+        torch.cuda.empty_cache()
+        extra["qwen_gdn"] = gdn_refresh_keys(torch, args)
+        torch.cuda.empty_cache()
+
+    # 3. the headline: warmup, then exactly args.steps timed steps
+    ms_step = timed_steps(torch, step, args)
+
     achieved = bytes_refresh / t["refresh"] / 1e6          # GB/s
-    traffic = measured_traffic("kimi_headline/refresh")
     out = {
         "metric": METRIC,
         "value": n_req * W / (ms_step / 1e3),
@@ -346,155 +339,167 @@ def bench_headline(torch, args):
         },
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": traffic, "kernel": "refresh",
+                     "traffic": measured_traffic("kimi_headline/refresh"), "kernel": "refresh",
                      "work_per_launch": f"{bytes_refresh} B = per refreshed head: k, v (bf16), g, "
                                         "beta (fp32), restored state read, omitted rows written",
                      "mfma_frac": flops_refresh / (t["refresh"] / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
                      "mfma_busy": measured_util("kimi_headline/refresh", "mfma_busy"),
                      "valu_active": measured_util("kimi_headline/refresh", "valu_active")},
+        "first_pass_ms_per_step": first_ms,
         "kernels": kernels,
         "pack_restore_GBps": (bytes_pack + bytes_restore) / (t["pack"] + t["restore"]) / 1e6,
+        "extra": extra,
         "plan_host_ms": plan_s * 1e3,
     }
+    # 4. the oracle on the host cores
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_headline(wl, plan, states_np, inp, W, n_req)
     return out
 
 
-def cpu_baseline_headline(wl, plan, states_np, inp, W, n_req):
-    """The oracle, as it stands, on a bounded sample of the same step."""
-    from threadpoolctl import threadpool_limits
+# ---- CPU baseline: the oracle, as it stands ---------------------------------------------
+
+def _oracle_sample(wl, plan, states_np, inp, W, n_req, threads):
+    """Seconds the oracle takes on the bounded sample (pack and restore of every
+    checkpoint, refresh of half the requests), its work split over `threads` host threads:
+    checkpoints and (request, head) pairs are dealt to the threads, each of which calls the
+    oracle's own functions on its share (numpy releases the interpreter lock inside its
+    array loops, so the shares run in parallel)."""
+    from concurrent.futures import ThreadPoolExecutor
 
     from oracle import pack as OK
     from oracle import recurrence as OR
 
-    n_s, req_s = wl.n_ckpt, n_req // 2        # all checkpoints, half the requests
+    n_s, req_s = wl.n_ckpt, n_req // 2
     R = int(plan["n_rows"])
     words = states_np.reshape(states_np.shape[0], -1, wl.dv).view(np.uint32)
-    with threadpool_limits(1):
+    ck_parts = [list(range(n_s))[i::threads] for i in range(threads)]
+    pairs = [(n, h) for n in range(req_s) for h in range(wl.n_heads)]
+    pair_parts = [pairs[i::threads] for i in range(threads)]
+    sub = {key: val[:req_s] for key, val in inp.items()}
+
+    def pack_restore(ids):
+        ck = OK.pack(words, ids, plan["unit_row"], np.zeros((1, len(ids), R, wl.dv), np.uint32),
+                     list(range(len(ids))))
+        back = OK.restore(ck, list(range(len(ids))), plan["unit_row"],
+                          np.zeros((len(ids),) + words.shape[1:], np.uint32), list(range(len(ids))))
+        return back
+
+    layer = np.ascontiguousarray(
+        pack_restore(list(range(req_s))).view(np.float32).reshape(req_s, wl.n_heads, wl.dk, wl.dv))
+
+    def refresh(ps):
+        return OR.refresh(layer, plan["inv_row"], sub["k"], sub["v"], sub["g"], sub["beta"],
+                          wl.n_qk_heads, pairs=ps)
+
+    with ThreadPoolExecutor(threads) as ex:
         t0 = time.perf_counter()
-        ck = OK.pack(words, list(range(n_s)), plan["unit_row"],
-                     np.zeros((1, n_s, R, wl.dv), np.uint32), list(range(n_s)))
-        t_pack = time.perf_counter() - t0
+        list(ex.map(pack_restore, [p for p in ck_parts if p]))
+        t_pr = time.perf_counter() - t0
         t0 = time.perf_counter()
-        back = OK.restore(ck, list(range(n_s)), plan["unit_row"], np.zeros_like(words[:n_s]),
-                          list(range(n_s)))
-        t_restore = time.perf_counter() - t0
-        layer = back.view(np.float32).reshape(n_s, wl.n_heads, wl.dk, wl.dv)
-        pairs = [(n, h) for n in range(req_s) for h in range(wl.n_heads)]
-        sub = {key: val[:req_s] for key, val in inp.items()}
-        t0 = time.perf_counter()
-        OR.refresh(layer[:req_s], plan["inv_row"], sub["k"], sub["v"], sub["g"], sub["beta"],
-                   wl.n_qk_heads, pairs=pairs)
+        list(ex.map(refresh, [p for p in pair_parts if p]))
         t_ref = time.perf_counter() - t0
-    scale_ck = wl.n_ckpt / n_s
-    step_s = (t_pack + t_restore) * scale_ck + t_ref * n_req / req_s
-    return {"value": n_req * W / step_s, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"pack+restore all {n_s} checkpoints, refresh {req_s} of {n_req} requests "
-                      f"x 32 heads at W={W} (fp64 per-token form, vectorised over heads); the "
-                      "refresh time is scaled to all requests",
-            "sample_seconds": t_pack + t_restore + t_ref,
-            "host_cpus": os.cpu_count()}
+    return t_pr, t_ref
 
 
-def bench_pack_restore_only(torch, args, name):
-    """GB-scale pack + restore (full-model KDA set) for the HBM roofline."""
+def cpu_baseline_headline(wl, plan, states_np, inp, W, n_req):
+    """The oracle, as it stands, on a bounded sample of the same step, timed on one host
+    thread and on every host core this process may run on (at most MAX_POOL_THREADS)."""
+    from threadpoolctl import threadpool_limits
+
+    affinity = len(os.sched_getaffinity(0))
+    n_all = max(1, min(affinity, MAX_POOL_THREADS))
+    res = {}
+    with threadpool_limits(1):              # no BLAS threads on top of the pool
+        for threads in sorted({1, n_all}):
+            t_pr, t_ref = _oracle_sample(wl, plan, states_np, inp, W, n_req, threads)
+            step_s = t_pr + t_ref * n_req / (n_req // 2)
+            res[threads] = {"value": n_req * W / step_s, "sample_seconds": t_pr + t_ref}
+    best = res[n_all]
+    return {"value": best["value"], "unit": "tokens/s", "cores": n_all, "kind": "oracle",
+            "sample": f"pack+restore all {wl.n_ckpt} checkpoints, refresh {n_req // 2} of {n_req} "
+                      f"requests x 32 heads at W={W} (fp64 per-token form); the refresh time is "
+                      f"scaled to all requests; work dealt to {n_all} host threads",
+            "sample_seconds": best["sample_seconds"],
+            "one_thread": {"value": res[1]["value"], "sample_seconds": res[1]["sample_seconds"]},
+            "host_cpus": os.cpu_count(), "affinity_cpus": affinity}
+
+
+# ---- full-model KDA checkpoint set --------------------------------------------------------
+
+def full_model_keys(torch, args, layouts=("ragged", "q8", "padded")):
+    """Pack/restore of the full-model KDA set (24 layers x 32 heads, 256 checkpoints, T = 8
+    rank slices), per-kernel durations by batched HIP events; GB-scale, so the rates are
+    HBM rates."""
     import paper_2608_30386_amd as D
     from workloads import WORKLOADS, states_device
 
-    wl = WORKLOADS[name]
+    wl = WORKLOADS["kimi_model"]
     sh, plan, plan_s = _setup_plan(wl)
     R, rows, dv, n = int(plan["n_rows"]), sh.rows, sh.dv, wl.n_ckpt
     T, C = wl.n_ranks, int(plan["slice_rows"])
     states = states_device(wl, n, "cuda")
-    ckpt = torch.empty((T, n, C, dv), dtype=torch.float32, device="cuda")
     active = torch.empty_like(states)
     unit_row, inv_row = _i32(torch, plan["unit_row"]), _i32(torch, plan["inv_row"])
     ids = _i32(torch, np.arange(n))
-    timer = KernelTimer(torch)
-
-    def plain_step():
-        D.dasc_pack(sh, states, ids, unit_row, ckpt, ids, n_ranks=T, slice_rows=C)
-        D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R, n_ranks=T, slice_rows=C)
-
-    def step():
-        timer.run("pack", lambda: D.dasc_pack(sh, states, ids, unit_row, ckpt, ids, n_ranks=T,
-                                              slice_rows=C))
-        timer.run("restore", lambda: D.dasc_restore(sh, ckpt, ids, inv_row, active, ids,
-                                                    n_rows=R, n_ranks=T, slice_rows=C))
-
-    ms_step = timed_steps(torch, plain_step, args)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    timer.spans.clear()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
     bp = 2 * R * dv * 4 * n
     br = (R + rows) * dv * 4 * n
-    t = {k_: timer.mean_ms(k_) for k_ in ("pack", "restore")}
-    gbps = (bp + br) / (t["pack"] + t["restore"]) / 1e6
-    dom = "restore" if t["restore"] >= t["pack"] else "pack"
-    dom_bytes = br if dom == "restore" else bp
-    ach = dom_bytes / t[dom] / 1e6
+    kern = {}
+    if "ragged" in layouts:
+        ckpt = torch.empty((T, n, C, dv), dtype=torch.float32, device="cuda")
+        kern["pack"] = _rate(batched_ms(torch, lambda: D.dasc_pack(
+            sh, states, ids, unit_row, ckpt, ids, n_ranks=T, slice_rows=C), batches=5), bp)
+        kern["restore"] = _rate(batched_ms(torch, lambda: D.dasc_restore(
+            sh, ckpt, ids, inv_row, active, ids, n_rows=R, n_ranks=T, slice_rows=C), batches=5), br)
+        del ckpt
+    if "q8" in layouts:
+        q = torch.empty((n, R, dv), dtype=torch.int8, device="cuda")
+        s = torch.empty((n, R), dtype=torch.float32, device="cuda")
+        kern["pack_q8"] = _rate(batched_ms(torch, lambda: D.dasc_pack_q8(
+            sh, states, ids, unit_row, q, s, ids), batches=5), R * n * (dv * 4 + dv + 4))
+        kern["restore_q8"] = _rate(batched_ms(torch, lambda: D.dasc_restore_q8(
+            sh, q, s, ids, inv_row, active, ids, n_rows=R), batches=5), n * (R * (dv + 4) + rows * dv * 4))
+        del q, s
+    if "padded" in layouts:
+        r_max = int(plan["r_max_rows"])
+        off = _i32(torch, plan["layer_off_rows"])
+        ck_pad = torch.empty((sh.n_layers, n, r_max, dv), dtype=torch.float32, device="cuda")
+        kern["pack_padded"] = _rate(batched_ms(torch, lambda: D.dasc_pack_padded(
+            sh, states, ids, unit_row, off, ck_pad, ids), batches=5), bp)
+        kern["restore_padded"] = _rate(batched_ms(torch, lambda: D.dasc_restore_padded(
+            sh, ck_pad, ids, off, inv_row, active, ids, n_rows=R), batches=5), br)
+        del ck_pad
+    del states, active
+    return {"workload": f"{wl.n_layers} KDA layers x 32h x 128x128 fp32, {n} checkpoints, "
+                        f"R={R} of {rows} rows kept, T={T} rank slices",
+            "kernels": kern,
+            "pack_restore_GBps": (bp + br) / (kern["pack"]["ms"] + kern["restore"]["ms"]) / 1e6
+            if "ragged" in layouts else None,
+            "checkpoint_bytes": {"fp32": R * dv * 4, "q8": R * (dv + 4),
+                                 "padded": sh.n_layers * int(plan["r_max_rows"]) * dv * 4},
+            "plan_host_ms": plan_s * 1e3}
 
-    # INT8 checkpoints (App. E.1) on the same states, flat layout, timed separately
-    del ckpt
-    q = torch.empty((n, R, dv), dtype=torch.int8, device="cuda")
-    s = torch.empty((n, R), dtype=torch.float32, device="cuda")
-    for _ in range(args.warmup):
-        D.dasc_pack_q8(sh, states, ids, unit_row, q, s, ids)
-        D.dasc_restore_q8(sh, q, s, ids, inv_row, active, ids, n_rows=R)
-    torch.cuda.synchronize()
-    timer.spans.clear()
-    for _ in range(args.steps):
-        timer.run("pack_q8", lambda: D.dasc_pack_q8(sh, states, ids, unit_row, q, s, ids))
-        timer.run("restore_q8", lambda: D.dasc_restore_q8(sh, q, s, ids, inv_row, active, ids,
-                                                          n_rows=R))
-    torch.cuda.synchronize()
-    tq = {k_: timer.mean_ms(k_) for k_ in ("pack_q8", "restore_q8")}
-    bpq = R * n * (dv * 4 + dv + 4)               # read fp32 rows, write int8 rows + scales
-    brq = n * (R * (dv + 4) + rows * dv * 4)      # read int8 rows + scales, write fp32 states
 
-    # padded layout (App. B Scheme 1, the comparison layout): same rows moved, L * R_max
-    # rows reserved per checkpoint
-    del q, s
-    r_max = int(plan["r_max_rows"])
-    off = _i32(torch, plan["layer_off_rows"])
-    ck_pad = torch.empty((sh.n_layers, n, r_max, dv), dtype=torch.float32, device="cuda")
-    for _ in range(args.warmup):
-        D.dasc_pack_padded(sh, states, ids, unit_row, off, ck_pad, ids)
-        D.dasc_restore_padded(sh, ck_pad, ids, off, inv_row, active, ids, n_rows=R)
-    torch.cuda.synchronize()
-    timer.spans.clear()
-    for _ in range(args.steps):
-        timer.run("pack_padded", lambda: D.dasc_pack_padded(sh, states, ids, unit_row, off, ck_pad,
-                                                            ids))
-        timer.run("restore_padded", lambda: D.dasc_restore_padded(sh, ck_pad, ids, off, inv_row,
-                                                                  active, ids, n_rows=R))
-    torch.cuda.synchronize()
-    del ck_pad
-    tp = {k_: timer.mean_ms(k_) for k_ in ("pack_padded", "restore_padded")}
+def bench_full_model(torch, args):
+    import paper_2608_30386_amd as D
+    from workloads import WORKLOADS
+
+    res = full_model_keys(torch, args)
+    wl_sh, plan, _ = _setup_plan(WORKLOADS["kimi_model"])
+    k = res["kernels"]
+    dom = "restore" if k["restore"]["ms"] >= k["pack"]["ms"] else "pack"
     return {
-        "metric": "pack+restore GB/s (full-model KDA checkpoint set)", "value": gbps, "unit": "GB/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "metric": "pack+restore GB/s (full-model KDA checkpoint set)",
+        "value": res["pack_restore_GBps"], "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": k["pack"]["ms"] + k["restore"]["ms"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
-        "data": "synthetic",
-        "config": {"workload": f"{wl.n_layers} KDA layers x 32h x 128x128 fp32, {n} checkpoints, "
-                               f"R={R} of {rows} rows kept, T={T} rank slices"},
-        "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": ach / HBM_PEAK_GBPS, "traffic": measured_traffic(f"{name}/{dom}"),
-                     "kernel": dom},
-        "kernels": {k_: {"ms": tt[k_], "GBps": b / tt[k_] / 1e6,
-                         "hbm_frac": b / tt[k_] / 1e6 / HBM_PEAK_GBPS, "bytes": b}
-                    for tt, k_, b in ((t, "pack", bp), (t, "restore", br),
-                                      (tq, "pack_q8", bpq), (tq, "restore_q8", brq),
-                                      (tp, "pack_padded", bp), (tp, "restore_padded", br))},
-        "q8_checkpoint_bytes": R * (dv + 4), "fp32_checkpoint_bytes": R * dv * 4,
-        "padded_checkpoint_bytes": sh.n_layers * r_max * dv * 4,
-        "tp_stage1": tp_stage1(D, sh, plan, T),
-        "plan_host_ms": plan_s * 1e3,
+        "data": "synthetic", "config": {"workload": res["workload"]},
+        "roofline": {"bound": "hbm", "achieved": k[dom]["GBps"], "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": k[dom]["GBps"] / HBM_PEAK_GBPS,
+                     "traffic": measured_traffic(f"kimi_model/{dom}"), "kernel": dom},
+        "kernels": k, "checkpoint_bytes": res["checkpoint_bytes"],
+        "tp_stage1": tp_stage1(D, wl_sh, plan, 8), "plan_host_ms": res["plan_host_ms"],
     }
 
 
@@ -511,114 +516,91 @@ def tp_stage1(D, sh, plan, T):
             "moved_rows_permuted": over(res["rank_rows"])}
 
 
-def bench_gdn(torch, args):
-    """Qwen-GDN shape: pack/restore 128 checkpoints, refresh 8 requests x 36 layers."""
+# ---- Qwen-GDN ------------------------------------------------------------------------------
+
+def gdn_refresh_keys(torch, args, with_pack_restore=False, with_fused=False):
+    """Refresh of the omitted v-heads of 8 requests over all 36 GDN layers at W = 1024
+    (each layer: the factor launch and the recurrence launch), per-layer durations by
+    batched HIP events.  Inputs are drawn on the device."""
     import paper_2608_30386_amd as D
-    from workloads import WORKLOADS, log_lambda, refresh_inputs, states_device
+    from workloads import WORKLOADS, log_lambda, refresh_inputs_device, states_device
 
     wl = WORKLOADS["qwen_gdn"]
     sh, plan, plan_s = _setup_plan(wl)
-    R, rows, dv, n, W = int(plan["n_rows"]), sh.rows, sh.dv, wl.n_ckpt, args.W
-    states = states_device(wl, n, "cuda")
-    ckpt = torch.empty((n, R, dv), dtype=torch.float32, device="cuda")
-    active = torch.empty_like(states)
-    unit_row, inv_row = _i32(torch, plan["unit_row"]), _i32(torch, plan["inv_row"])
-    ids, req = _i32(torch, np.arange(n)), _i32(torch, np.arange(wl.n_req))
+    R, rows, dv, W, n_req = int(plan["n_rows"]), sh.rows, sh.dv, args.W, wl.n_req
+    n_pool = wl.n_ckpt if with_pack_restore else n_req
+    states = states_device(wl, n_pool, "cuda")
+    active = states.clone()
+    inv_row = _i32(torch, plan["inv_row"])
+    req = _i32(torch, np.arange(n_req))
     lam = log_lambda(wl)
-    layers = []
-    for l in range(wl.n_layers):
-        inp = refresh_inputs(wl, W, lam[l], salt=l)
-        layers.append((_bf16(torch, inp["k"]), _bf16(torch, inp["v"]),
-                       torch.from_numpy(inp["g"]).cuda(), torch.from_numpy(inp["beta"]).cuda()))
-    # the per-chunk WY factors of the two-launch GDN kernel, allocated once
-    ws = torch.empty(D.dasc_refresh_workspace_bytes(sh, wl.n_req, W), dtype=torch.uint8,
-                     device="cuda")
-    timer = KernelTimer(torch)
+    layers = [refresh_inputs_device(wl, W, lam[l], "cuda", salt=l) for l in range(wl.n_layers)]
+    ws = torch.empty(D.dasc_refresh_workspace_bytes(sh, n_req, W), dtype=torch.uint8, device="cuda")
 
-    def ref():
-        for l, (k, v, g, b) in enumerate(layers):
-            D.dasc_refresh(sh, l, inv_row, active, req, k, v, g, b, W, workspace=ws)
+    def ref_all():
+        for l, x in enumerate(layers):
+            D.dasc_refresh(sh, l, inv_row, active, req, x["k"], x["v"], x["g"], x["beta"], W,
+                           workspace=ws)
 
-    def plain_step():
-        D.dasc_pack(sh, states, ids, unit_row, ckpt, ids)
-        D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R)
-        ref()
-
-    def step():
-        timer.run("pack", lambda: D.dasc_pack(sh, states, ids, unit_row, ckpt, ids))
-        timer.run("restore", lambda: D.dasc_restore(sh, ckpt, ids, inv_row, active, ids, n_rows=R))
-        timer.run("refresh_all_layers", ref)
-
-    ms_step = timed_steps(torch, plain_step, args)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    timer.spans.clear()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-
-    # Load with refresh of the 8 requests: dasc_restore of their states + the 36 layer
-    # refreshes, against one dasc_restore_refresh per layer (each restores its own layer;
-    # the same bits)
-    def load_wr():
-        timer.run("restore_req", lambda: D.dasc_restore(sh, ckpt, req, inv_row, active, req, n_rows=R))
-        timer.run("refresh_req", ref)
-
-        def fused():
-            for l, (k, v, g, b) in enumerate(layers):
-                D.dasc_restore_refresh(sh, l, ckpt, req, inv_row, active, req, k, v, g, b, W, n_rows=R,
-                                       workspace=ws)
-        timer.run("restore_refresh", fused)
-
-    load_wr()
-    torch.cuda.synchronize()
-    for name in ("restore_req", "refresh_req", "restore_refresh"):
-        timer.spans[name].clear()
-    for _ in range(args.steps):
-        load_wr()
-    torch.cuda.synchronize()
-    t = {k_: timer.mean_ms(k_) for k_ in ("pack", "restore", "refresh_all_layers", "restore_req",
-                                          "refresh_req", "restore_refresh")}
-    bp, br = 2 * R * dv * 4 * n, (R + rows) * dv * 4 * n
+    ms_all = batched_ms(torch, ref_all, batches=5, per_batch=4)
     omitted = (plan["inv_row"].reshape(sh.n_layers, sh.n_heads, sh.dk) < 0).all(axis=2)
-    om_heads = int(omitted.sum())
-    heads = wl.n_req * om_heads
+    heads = n_req * int(omitted.sum())
     # key heads some omitted v-head of their layer reads (v-heads of a group share one)
-    key_heads = wl.n_req * sum(len(set(np.flatnonzero(o) // (sh.n_heads // sh.n_qk_heads)))
-                               for o in omitted)
+    key_heads = n_req * sum(len(set(np.flatnonzero(o) // (sh.n_heads // sh.n_qk_heads)))
+                            for o in omitted)
     # per refreshed head: v (bf16), g, beta (fp32), the restored head read and written; per
     # key head read: k (bf16)
     per_head = 2 * W * dv + 4 * W + 4 * W + 2 * 4 * sh.dk * dv
     bytes_ref = heads * per_head + key_heads * 2 * W * sh.dk
-    ach = bytes_ref / (t["refresh_all_layers"] / 1e3) / 1e9          # GB/s
-    flops = 5.0 * sh.dk * dv * W * heads
+    out = {"workload": f"Qwen-GDN 36 layers, 16 qk / 32 v heads 128x128: refresh {n_req} requests "
+                       f"x {heads // n_req // wl.n_layers} omitted heads per layer, W={W}",
+           "refresh_all_layers": {"tokens_per_s": n_req * W / (ms_all / 1e3), "launches": 2 * wl.n_layers,
+                                  "per_layer_ms": ms_all / wl.n_layers, **_rate(ms_all, bytes_ref)},
+           "bytes_per_layer": bytes_ref // wl.n_layers,
+           "recurrence_TFLOPs": 5.0 * sh.dk * dv * W * heads / (ms_all / 1e3) / 1e12,
+           "plan_host_ms": plan_s * 1e3}
+    if with_fused:
+        ckpt = torch.empty((n_pool, R, dv), dtype=torch.float32, device="cuda")
+        ids = _i32(torch, np.arange(n_pool))
+        D.dasc_pack(sh, states, ids, _i32(torch, plan["unit_row"]), ckpt, ids)
+
+        def fused():
+            for l, x in enumerate(layers):
+                D.dasc_restore_refresh(sh, l, ckpt, req, inv_row, active, req, x["k"], x["v"], x["g"],
+                                       x["beta"], W, n_rows=R, workspace=ws)
+        t_restore = batched_ms(torch, lambda: D.dasc_restore(sh, ckpt, req, inv_row, active, req,
+                                                             n_rows=R), batches=5)
+        out["restore_refresh_fused"] = {"ms": batched_ms(torch, fused, batches=5, per_batch=4),
+                                        "unfused_ms": t_restore + ms_all, "requests": n_req}
+    if with_pack_restore:
+        ckpt = torch.empty((n_pool, R, dv), dtype=torch.float32, device="cuda")
+        ids = _i32(torch, np.arange(n_pool))
+        unit_row = _i32(torch, plan["unit_row"])
+        out["pack"] = _rate(batched_ms(torch, lambda: D.dasc_pack(sh, states, ids, unit_row, ckpt, ids),
+                                       batches=5), 2 * R * dv * 4 * n_pool)
+        out["restore"] = _rate(batched_ms(torch, lambda: D.dasc_restore(
+            sh, ckpt, ids, inv_row, active, ids, n_rows=R), batches=5), (R + rows) * dv * 4 * n_pool)
+    del states, active, layers, ws
+    return out
+
+
+def bench_gdn(torch, args):
+    """Qwen-GDN shape: refresh 8 requests x 36 layers, fused Load, pack/restore 128
+    checkpoints."""
+    res = gdn_refresh_keys(torch, args, with_pack_restore=True, with_fused=True)
+    r = res["refresh_all_layers"]
     return {
-        "metric": "GDN pack/restore GB/s + refresh tokens/s (36 layers)",
-        "value": wl.n_req * W / (t["refresh_all_layers"] / 1e3), "unit": "tokens/s (all 36 layers)",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "metric": "GDN refresh tokens/s (36 layers) + pack/restore GB/s",
+        "value": r["tokens_per_s"], "unit": "tokens/s (all 36 layers)",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": r["ms"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic",
-        "config": {"workload": f"Qwen-GDN 36 layers 16 qk / 32 v heads 128x128: pack+restore {n} "
-                               f"checkpoints (12 of 32 heads kept), refresh {wl.n_req} requests x "
-                               f"{om_heads} omitted heads W={W}"},
-        "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": ach / HBM_PEAK_GBPS, "traffic": measured_traffic("qwen_gdn/refresh"),
-                     "kernel": "refresh",
-                     "work_per_launch": f"{bytes_ref // wl.n_layers} B per layer launch "
-                                        f"({heads // wl.n_layers} heads, "
-                                        f"{key_heads / wl.n_layers:.1f} key heads)",
-                     "recurrence_TFLOPs": flops / (t["refresh_all_layers"] / 1e3) / 1e12,
+        "data": "synthetic", "config": {"workload": res["workload"]},
+        "roofline": {"bound": "hbm", "achieved": r["GBps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": r["hbm_frac"], "traffic": measured_traffic("qwen_gdn/refresh"),
+                     "kernel": "refresh (factor + recurrence per layer)",
                      "mfma_busy": measured_util("qwen_gdn/refresh", "mfma_busy"),
                      "valu_active": measured_util("qwen_gdn/refresh", "valu_active")},
-        "kernels": {"pack": {"ms": t["pack"], "GBps": bp / t["pack"] / 1e6},
-                    "restore": {"ms": t["restore"], "GBps": br / t["restore"] / 1e6},
-                    "refresh_all_layers": {"ms": t["refresh_all_layers"], "GBps": ach,
-                                           "launches": 2 * wl.n_layers, "bytes": bytes_ref},
-                    "restore_refresh_fused": {"ms": t["restore_refresh"], "launches": 2 * wl.n_layers,
-                                              "unfused_ms": t["restore_req"] + t["refresh_req"],
-                                              "requests": wl.n_req}},
-        "plan_host_ms": plan_s * 1e3,
+        "kernels": res,
     }
 
 

@@ -13,6 +13,7 @@ from .synth import (  # noqa: F401
     f32_from_bf16_bits,
     log_lambda,
     refresh_inputs,
+    refresh_inputs_device,
     states_host,
     states_device,
     streams,

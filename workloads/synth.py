@@ -243,3 +243,32 @@ def refresh_inputs(wl: Workload, W: int, lam_layer: np.ndarray, n_req: int | Non
         "g": np.ascontiguousarray(g),
         "beta": np.ascontiguousarray(beta),
     }
+
+
+def refresh_inputs_device(wl: Workload, W: int, lam_layer: np.ndarray, device,
+                          n_req: int | None = None, salt: int = 0) -> dict:
+    """refresh_inputs' recipe drawn directly in device memory with torch's seeded
+    generator, for benchmark inputs too large to draw on the host quickly.  Same shapes,
+    dtypes and distributions (keys L2-normalised in fp32 then rounded to bf16 by
+    round-to-nearest-even, values rounded the same way, g = -lambda * softplus(z),
+    beta = sigmoid(N(0, 1))); not the same bits as the host recipe.  Returns device
+    tensors: k, v bfloat16; g, beta float32."""
+    import torch
+
+    n_req = wl.n_req if n_req is None else n_req
+    H, Hqk, dk, dv = wl.n_heads, wl.n_qk_heads, wl.dk, wl.dv
+    gen = torch.Generator(device=device)
+    gen.manual_seed(wl.seed * 1_000_003 + 104_729 * (salt + 1) + 31 * W)
+    k = torch.randn((n_req, Hqk, W, dk), generator=gen, device=device)
+    k = (k / torch.sqrt((k * k).sum(dim=-1, keepdim=True))).to(torch.bfloat16)
+    v = torch.randn((n_req, H, W, dv), generator=gen, device=device).to(torch.bfloat16)
+    lam = torch.exp(torch.as_tensor(np.asarray(lam_layer, dtype=np.float64))).to(torch.float32)
+    if wl.arch == "kda":
+        z = torch.randn((n_req, H, W, dk), generator=gen, device=device)
+        lam_b = lam.to(device)[None, :, None, :]
+    else:
+        z = torch.randn((n_req, H, W), generator=gen, device=device)
+        lam_b = lam.to(device)[None, :, None]
+    g = (-lam_b * torch.nn.functional.softplus(z)).contiguous()
+    beta = torch.sigmoid(torch.randn((n_req, H, W), generator=gen, device=device)).contiguous()
+    return {"k": k.contiguous(), "v": v.contiguous(), "g": g, "beta": beta}
