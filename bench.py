@@ -15,16 +15,19 @@ time (n_req * W / step time); per-kernel rates are in `kernels`.  All inputs are
 resident in HBM before any timed region starts.
 
 Order of work on the GPU:
+  0. the headline measurement below taken as the very first GPU work of the process,
+     reported as `first_pass_ms_per_step`;
   1. per-kernel durations of the step's kernels, from HIP events around batches of
      back-to-back launches of one kernel (median over batches);
-  2. the other configurations, as extra keys: the full-model KDA checkpoint set (24
+  2. the headline: --warmup untimed steps, then exactly --steps timed steps between
+     two synchronisations.  The refresh kernel's own duration drifts with the GPU's
+     clock under sustained load (in a kernel trace of one run: ~306 us for the first
+     launches, up to ~350 us within ten steps, then down to ~270 us after a few hundred
+     launches), so a short timed region measured first thing reads ~15% slower per step
+     than the same region after step 1;
+  3. the other configurations, as extra keys: the full-model KDA checkpoint set (24
      layers, 256 checkpoints, T = 8 rank slices) pack/restore, and the Qwen-GDN refresh
      of 8 requests x 36 layers (`extra`);
-  3. the headline: --warmup untimed steps, then exactly --steps timed steps between
-     two synchronisations.  From an idle GPU the clock takes ~25 back-to-back steps to
-     settle under this load; by the time step 3 runs, steps 1-2 have kept the GPU busy
-     for several seconds.  `first_pass_ms_per_step` is the same measurement taken as
-     the very first GPU work of the process (cold clock), for comparison;
   4. the CPU baseline (the oracle on the host cores, at 1 thread and at all of them).
 
     python bench.py [--steps K] [--warmup W] [--workload kimi_headline|kimi_model|qwen_gdn]
@@ -310,16 +313,16 @@ def bench_headline(torch, args):
         "timing": "HIP events around 10 batches of 10 back-to-back launches, median",
     }
 
-    # 2. the other configurations
+    # 2. the headline: warmup, then exactly args.steps timed steps
+    ms_step = timed_steps(torch, step, args)
+
+    # 3. the other configurations
     extra = {}
     if not args.no_extra:
         extra["kimi_model"] = full_model_keys(torch, args, layouts=("ragged",))
         torch.cuda.empty_cache()
         extra["qwen_gdn"] = gdn_refresh_keys(torch, args)
         torch.cuda.empty_cache()
-
-    # 3. the headline: warmup, then exactly args.steps timed steps
-    ms_step = timed_steps(torch, step, args)
 
     achieved = bytes_refresh / t["refresh"] / 1e6          # GB/s
     out = {

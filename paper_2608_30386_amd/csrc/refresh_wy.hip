@@ -42,10 +42,12 @@
 //
 // Fused with the restore (FUSED = true), the initial state of a head is read from the
 // packed checkpoint instead of the active state (kept rows from their packed position,
-// omitted rows +0.0), and every row of the layer is written: kept rows, copied bit for
-// bit from the checkpoint, as soon as they are read (they overlap the replay), omitted
-// rows from the replay at the end.  A head with no omitted row is a plain copy.  The arithmetic is the unfused kernel's, so the result
-// equals restore followed by refresh bit for bit.
+// omitted rows +0.0), and every row of the layer is written: kept rows first, copied bit
+// for bit from the checkpoint in one 16-byte-per-thread pass whose stores drain while the
+// replay runs, omitted rows from the replay at the end.  A head with no omitted row is a
+// plain copy.  The arithmetic is the unfused kernel's, so the result equals restore
+// followed by refresh bit for bit.  (Storing the kept rows from the registers that load
+// the initial state instead keeps those values live into the replay and makes it spill.)
 //
 // Inputs are read through raw buffer resources sized to one head's window, so tokens
 // past the window load as zeros: k = v = 0, g = 0, beta = 0, an identity step.
@@ -146,37 +148,40 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     if (tid < D) sOff[tid] = dasc::ckpt_row_offset(inv_row[head_row + tid], ck, cslot, D);
     __syncthreads();
   }
-  if (FUSED && !any_omitted) {   // nothing to replay: restore the head as it is
+  if (FUSED) {
+    // Every row that is not replayed is final already: its checkpoint row (or +0.0) is
+    // copied to the pool here, 16 bytes per thread and access, and the stores drain
+    // while the replay runs.  A head with no omitted row is done after this.
     for (int e = tid; e < D * D / 4; e += 256) {
       const int c = e >> 5, v4 = e & 31;
       const int64_t o = sOff[c];
-      const f32x4 val = o >= 0 ? reinterpret_cast<const f32x4*>(ck.ckpt + o)[v4]
-                               : f32x4{0.f, 0.f, 0.f, 0.f};
-      reinterpret_cast<f32x4*>(S_head + int64_t(c) * D)[v4] = val;
+      if (!any_omitted || o != kOmitted) {
+        const f32x4 val = o >= 0 ? reinterpret_cast<const f32x4*>(ck.ckpt + o)[v4]
+                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+        reinterpret_cast<f32x4*>(S_head + int64_t(c) * D)[v4] = val;
+      }
     }
-    return;
+    if (!any_omitted) return;
   }
 
-  // S'[c][j] for c = 16 mt + 4q + i, j = 32w + 16 nt + r
+  // S'[c][j] for c = 16 mt + 4q + i, j = 32w + 2r + nt: the lane's two columns of a row
+  // are adjacent, one 8-byte load
   f32x4 S[8][2];
 #pragma unroll
   for (int mt = 0; mt < 8; ++mt)
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int c = 16 * mt + 4 * q + i, j = 32 * w + 2 * r + nt;
-        if (FUSED) {
-          // the restored value; a kept row is final already and is stored right away,
-          // while the replay runs
-          const int64_t o = sOff[c];
-          const float val = o >= 0 ? ck.ckpt[o + j] : 0.f;
-          S[mt][nt][i] = init_zero ? 0.f : val;
-          if (o != kOmitted) S_head[int64_t(c) * D + j] = val;
-        } else {
-          S[mt][nt][i] = init_zero ? 0.f : S_head[int64_t(c) * D + j];
-        }
+    for (int i = 0; i < 4; ++i) {
+      const int c = 16 * mt + 4 * q + i, j = 32 * w + 2 * r;
+      f32x2 val = {0.f, 0.f};
+      if (FUSED) {
+        const int64_t o = sOff[c];   // the restored value: kept row, or +0.0
+        if (!init_zero && o >= 0) val = *reinterpret_cast<const f32x2*>(ck.ckpt + o + j);
+      } else if (!init_zero) {
+        val = *reinterpret_cast<const f32x2*>(S_head + int64_t(c) * D + j);
       }
+      S[mt][0][i] = val[0];
+      S[mt][1][i] = val[1];
+    }
 
   const int hk = h / (H / Hqk);
   const uint16_t* kp = k + (int64_t(n) * Hqk + hk) * W * D;
@@ -260,10 +265,8 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       const int rf = w == 0 ? 8 : (w == 1 ? 15 : 24);   // reference token of the tile
       const int tr = 16 * ti + r, sr = 16 * si + r;
       f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
-      // fully unrolled the reads and exponentials overlap best; the fused variant keeps
-      // two steps, where the checkpoint row table already presses on registers
-      constexpr int kAUnroll = FUSED ? 2 : 4;
-#pragma unroll kAUnroll
+      // fully unrolled: the reads and exponentials overlap best
+#pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const int c0 = 32 * kk + 8 * q;
         float fa[8], fb[8];
