@@ -283,15 +283,20 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
     if (tid < D) sOff[tid] = dasc::ckpt_row_offset(inv_row[head_row + tid], ck, cslot, D);
     __syncthreads();
   }
-  if (FUSED && !any_omitted) {   // nothing to replay: restore this half of the columns
+  if (FUSED) {
+    // Rows that are not replayed (this half of their columns) are final already: copied
+    // from the checkpoint (or +0.0) in one 16-byte-per-thread pass, whose stores drain
+    // while the replay runs.  A head with no omitted row is done after this.
     for (int e = tid; e < D * DH / 4; e += 256) {
       const int c = e / (DH / 4), v4 = e % (DH / 4);
       const int64_t o = sOff[c];
-      const f32x4 val = o >= 0 ? reinterpret_cast<const f32x4*>(ck.ckpt + o + DH * half)[v4]
-                               : f32x4{0.f, 0.f, 0.f, 0.f};
-      reinterpret_cast<f32x4*>(S_head + int64_t(c) * D + DH * half)[v4] = val;
+      if (!any_omitted || o != dasc::kOmitted) {
+        const f32x4 val = o >= 0 ? reinterpret_cast<const f32x4*>(ck.ckpt + o + DH * half)[v4]
+                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+        reinterpret_cast<f32x4*>(S_head + int64_t(c) * D + DH * half)[v4] = val;
+      }
     }
-    return;
+    if (!any_omitted) return;
   }
 
   // S'[c][col] for c = 16 mt + 4q + i
@@ -301,14 +306,14 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int c = 16 * mt + 4 * q + i;
+      float val = 0.f;
       if (FUSED) {
-        const int64_t o = sOff[c];
-        const float val = o >= 0 ? ck.ckpt[o + col] : 0.f;
-        S[mt][i] = init_zero ? 0.f : val;
-        if (o != dasc::kOmitted) S_head[int64_t(c) * D + col] = val;
-      } else {
-        S[mt][i] = init_zero ? 0.f : S_head[int64_t(c) * D + col];
+        const int64_t o = sOff[c];   // the restored value: kept row, or +0.0
+        if (!init_zero && o >= 0) val = ck.ckpt[o + col];
+      } else if (!init_zero) {
+        val = S_head[int64_t(c) * D + col];
       }
+      S[mt][i] = val;
     }
 
   const int hk = h / (H / Hqk);
