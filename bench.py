@@ -65,6 +65,9 @@ def parse():
     ap.add_argument("--workload", default="kimi_headline",
                     choices=["kimi_headline", "kimi_model", "qwen_gdn"])
     ap.add_argument("--W", type=int, default=1024)
+    ap.add_argument("--batches", type=int, default=10,
+                    help="per-kernel timing: batches of back-to-back launches (median over them)")
+    ap.add_argument("--per-batch", type=int, default=10, help="launches per timing batch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
                     help="headline only: skip the full-model KDA and Qwen-GDN extra keys")
@@ -112,11 +115,17 @@ def measured_util(key: str, what: str):
     return _counter_summary().get("utilisation", {}).get(key, {}).get(what)
 
 
-def batched_ms(torch, fn, batches: int = 10, per_batch: int = 10, warm: int = 3) -> float:
+BATCHES, PER_BATCH = 10, 10   # set from --batches / --per-batch
+
+
+def batched_ms(torch, fn, batches: int | None = None, per_batch: int | None = None,
+               warm: int = 3) -> float:
     """Duration of one call of `fn` on the GPU (ms): HIP events on torch's current stream
     (the stream the library launches on) around `batches` runs of `per_batch`
     back-to-back calls, the median over the batches of elapsed / per_batch.  Events around
     whole batches add no per-launch gap."""
+    batches = BATCHES if batches is None else min(batches, BATCHES)
+    per_batch = PER_BATCH if per_batch is None else min(per_batch, PER_BATCH)
     for _ in range(warm):
         fn()
     spans = []
@@ -154,7 +163,9 @@ def copy_bandwidth(torch, args):
 
 
 def main():
+    global BATCHES, PER_BATCH
     args = parse()
+    BATCHES, PER_BATCH = max(1, args.batches), max(1, args.per_batch)
     if args.gpus != 1:
         print("bench.py measures one GPU: the library has no multi-GPU path "
               "(the checkpoint kernels run on one device). Use --gpus 1.", file=sys.stderr)

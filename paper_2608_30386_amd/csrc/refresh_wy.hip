@@ -32,13 +32,18 @@
 // LDS rows are padded so that the 16 (or 32) rows touched by one access instruction
 // fall on distinct banks; every operand is read as a 16- or 8-byte vector.
 //
-// Decay factors.  exp(G_t - G_s) <= 1 for s <= t, but the factorised form needs
-// exp(G_t - G_ref) exp(G_ref - G_s).  Off-diagonal 16-token blocks use the block
-// boundary as reference (both factors <= 1); diagonal blocks use the block midpoint,
-// whose factors are bounded by exp(8 |g|max).  Per-token log-gates are therefore
-// floored at -10 (a decay of 4.5e-5 per token instead of anything smaller), which
-// keeps every factor below e^80 in fp32 and changes the state by at most 4.5e-5 of
-// its magnitude per floored token.
+// Decay factors.  exp(G_t - G_s) <= 1 for s <= t, but a factorised form needs
+// exp(G_t - G_ref) exp(G_ref - G_s).  Fast path: when every channel decays by at most
+// 2^96 over the chunk (a block-wide test per chunk; realistic gates decay far less),
+// the reference is the chunk start: A = Diag(beta) strictly-lower(K_G Q^T) with
+// K_G = k 2^G (which X needs anyway) and Q = k 2^{-G} <= 2^96 |k|, so the chunk takes
+// two exponentials per (token, channel) for A and one for K_H, all formed by the thread
+// that holds the gates in registers.  Strong-decay path otherwise: off-diagonal 16-token
+// blocks use the block boundary as reference (both factors <= 1); diagonal blocks use the
+// block midpoint, whose factors are bounded by exp(8 |g|max).  Per-token log-gates are
+// floored at -10 (a decay of 4.5e-5 per token instead of anything smaller), which keeps
+// every factor below e^80 in fp32 and changes the state by at most 4.5e-5 of its
+// magnitude per floored token.
 //
 // Fused with the restore (FUSED = true), the initial state of a head is read from the
 // packed checkpoint instead of the active state (kept rows from their packed position,
@@ -67,6 +72,9 @@ using namespace dasc_wy;
 constexpr int C = 32;       // tokens per chunk
 constexpr int D = 128;      // dk = dv
 constexpr float kGateFloor = -10.f;
+// Fast path bound: every channel's log2-decay over a chunk at least -kFastRange, so that
+// k 2^G and k 2^{-G} stay normal fp32 (and their bf16 low parts too) for every token.
+constexpr float kFastRange = 96.f;
 constexpr float kLog2e = 1.4426950408889634f;
 
 // padded row strides (elements)
@@ -76,9 +84,10 @@ constexpr int SV = 40;      // bf16 [D][SV]  K_H^T
 constexpr int SP = 36;      // bf16 [C][SP]  T' (8-byte aligned rows)
 
 // LDS map (bytes).  The key buffer is dead once A and K_H are built and then holds
-// T and T'.
-constexpr int OFF_G = 0;                       // f32  [C][SG]
-constexpr int OFF_K = OFF_G + C * SG * 4;      // bf16 [C][SK]  -> later T, T'
+// T and T'.  On the fast path the gate buffer holds Q (hi, lo) instead.
+constexpr int G_BYTES = C * SG * 4 > 2 * C * SK * 2 ? C * SG * 4 : 2 * C * SK * 2;
+constexpr int OFF_G = 0;                       // f32  [C][SG]; fast path: bf16 [2][C][SK] Q
+constexpr int OFF_K = OFF_G + G_BYTES;         // bf16 [C][SK]  -> later T, T'
 constexpr int OFF_T = OFF_K;                   // f32  [C][C]
 constexpr int OFF_TPH = OFF_K + C * C * 4;     // bf16 [C][SP]
 constexpr int OFF_TPL = OFF_TPH + C * SP * 2;
@@ -89,7 +98,8 @@ constexpr int OFF_KHL = OFF_KHH + D * SV * 2;
 constexpr int OFF_A = OFF_KHL + D * SV * 2;    // f32  [C][C]
 constexpr int OFF_BETA = OFF_A + C * C * 4;    // f32  [C]
 constexpr int OFF_GAM = OFF_BETA + C * 4;      // f32  [D] exp(G_C)
-constexpr int LDS_BYTES = OFF_GAM + D * 4;
+constexpr int OFF_FLAGS = OFF_GAM + D * 4;     // int  [4] per wave: fast path possible
+constexpr int LDS_BYTES = OFF_FLAGS + 4 * 4;
 static_assert(C * C * 4 + 2 * C * SP * 2 <= C * SK * 2, "T and T' must fit in the key buffer");
 static_assert(LDS_BYTES <= 81920, "two blocks per CU");
 
@@ -117,6 +127,9 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   __bf16* sTPL = reinterpret_cast<__bf16*>(smem + OFF_TPL);
   float* sBeta = reinterpret_cast<float*>(smem + OFF_BETA);
   float* sGam = reinterpret_cast<float*>(smem + OFF_GAM);
+  int* sFast = reinterpret_cast<int*>(smem + OFF_FLAGS);
+  __bf16* sQH = reinterpret_cast<__bf16*>(smem + OFF_G);   // fast path only
+  __bf16* sQL = sQH + C * SK;
 
   const int n = blockIdx.x / H;
   const int h = blockIdx.x - n * H;
@@ -191,26 +204,31 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   const __amdgpu_buffer_rsrc_t rk = rsrc(kp, W * D * 2), rv = rsrc(vp, W * D * 2);
   const __amdgpu_buffer_rsrc_t rg = rsrc(gp, PER_CHANNEL ? W * D * 4 : W * 4), rb = rsrc(bp, W * 4);
 
-  // Load phase: lane pair (2 ch, 2 ch + 1) owns channel ch, the even lane tokens
-  // 0..15 of the chunk and the odd lane tokens 16..31, so the running sum of the gates
-  // crosses the halves with one lane shuffle.
-  const int ch = tid >> 1;
-  const int hf = tid & 1;
+  // Load phase: thread (cq = tid / 8, og = tid % 8) owns channels 4 cq .. 4 cq + 3 at the
+  // four tokens 4 og .. 4 og + 3 of a chunk.  It loads their gates and keys one chunk
+  // ahead and forms the running sums of the gates (the eight token groups of a channel
+  // quad are eight adjacent lanes); on the fast path it also builds their entries of K_G,
+  // Q and K_H from its registers, each written as one 8-byte store per token or channel
+  // (a wave's stores then fall on distinct LDS banks).
+  const int cq = tid >> 3, og = tid & 7;
+  const int c4 = 4 * cq, t4 = 4 * og;
 
   // Gates, keys and beta of one chunk as this thread loads them; the next chunk's are
   // issued one chunk ahead.
-  float graw[16];
-  uint4 kraw[2];
+  f32x4 graw[4];
+  uint2 kq[4];
   float braw;
   auto fetch = [&](int c0) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      graw[i] = PER_CHANNEL ? ldf(rg, ((16 * hf + i) * D + ch) * 4, c0 * D * 4)
-                            : ldf(rg, (16 * hf + i) * 4, c0 * 4);
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
-      kraw[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, (t * D + c8) * 2, c0 * D * 2, 0));
+    for (int i = 0; i < 4; ++i) {
+      if (PER_CHANNEL) {
+        graw[i] = ldf4(rg, ((t4 + i) * D + c4) * 4, c0 * D * 4);
+      } else {
+        const float x = ldf(rg, (t4 + i) * 4, c0 * 4);
+        graw[i] = f32x4{x, x, x, x};
+      }
+      kq[i] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
+                                            rk, ((t4 + i) * D + c4) * 2, c0 * D * 2, 0));
     }
     braw = ldf(rb, (tid & (C - 1)) * 4, c0 * 4);
   };
@@ -227,135 +245,270 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         vreg[mu][i] = __builtin_amdgcn_raw_buffer_load_b32(
             rv, ((16 * mu + 4 * q + i) * D + 32 * w + 2 * r) * 2, c0 * D * 2, 0);
   };
+  // X = K_G S' on this wave's columns (rows t, contraction over channels)
+  f32x4 X[2][2];
+  auto x_phase = [&]() {
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu)
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) X[mu][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      bf16x8 sh[2], slo[2];
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = S[2 * kk + (e >> 2)][nt][e & 3];
+        split8(x, sh[nt], slo[nt]);
+      }
+#pragma unroll
+      for (int mu = 0; mu < 2; ++mu) {
+        const int o = (16 * mu + r) * SK + 32 * kk + 4 * q;
+        const bf16x8 ah = ld_op(sKGH + o), al = ld_op(sKGL + o);
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) X[mu][nt] = mma3(ah, al, sh[nt], slo[nt], X[mu][nt]);
+      }
+    }
+  };
   fetch(0);
   fetch_v(0);
 
   for (int t0 = 0; t0 < W; t0 += C) {
-    // ---- stage the prefetched gates (running sums), keys and beta -----------------------
-    float Gl[16];
+    // ---- stage the prefetched gates (running sums) and beta ------------------------------
+    f32x4 Gl[4];   // G at tokens t4 + i, channels c4 .. c4 + 3
+    f32x4 gc;      // G at the chunk's last token
     {
-      float run = 0.f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        run += fmaxf(graw[i], kGateFloor) * kLog2e;
-        Gl[i] = run;
-      }
-      const float other = __shfl_xor(run, 1);   // every lane takes part
-      const float base = hf ? other : 0.f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) Gl[i] += base;
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
-      *reinterpret_cast<uint4*>(sK + t * SK + c8) = kraw[u];
-    }
-    if (tid < C) sBeta[tid] = braw;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) sG[(16 * hf + i) * SG + ch] = Gl[i];
-    if (hf) sGam[ch] = ex2(Gl[15]);
-    __syncthreads();
-
-    // ---- A = Diag(beta) (strictly lower part of R Q^T), three 16x16 tiles -----------
-    // bf16 MFMA (16x16x32) on hi/lo split factors, like the state products: lane (q, r)
-    // feeds channels 32 kk + 8 q + e of its row to step kk (three MFMAs a step where fp32
-    // MFMA would take eight, at a sixteenth of the bf16 rate).
-    if (w < 3) {
-      const int ti = w == 0 ? 0 : 1, si = w == 2 ? 1 : 0;
-      const int rf = w == 0 ? 8 : (w == 1 ? 15 : 24);   // reference token of the tile
-      const int tr = 16 * ti + r, sr = 16 * si + r;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
-      // fully unrolled: the reads and exponentials overlap best
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int c0 = 32 * kk + 8 * q;
-        float fa[8], fb[8];
-#pragma unroll
-        for (int h2 = 0; h2 < 2; ++h2) {
-          const f32x4 gt = *reinterpret_cast<const f32x4*>(sG + tr * SG + c0 + 4 * h2);
-          const f32x4 gs = *reinterpret_cast<const f32x4*>(sG + sr * SG + c0 + 4 * h2);
-          const f32x4 gf = *reinterpret_cast<const f32x4*>(sG + rf * SG + c0 + 4 * h2);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            fa[4 * h2 + i] = ex2(gt[i] - gf[i]);
-            fb[4 * h2 + i] = ex2(gf[i] - gs[i]);
-          }
-        }
-        const uint4 kt = *reinterpret_cast<const uint4*>(sK + tr * SK + c0);
-        const uint4 ks = *reinterpret_cast<const uint4*>(sK + sr * SK + c0);
-        const uint32_t ktw[4] = {kt.x, kt.y, kt.z, kt.w}, ksw[4] = {ks.x, ks.y, ks.z, ks.w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          fa[e] *= __uint_as_float((e & 1) ? (ktw[e >> 1] & 0xFFFF0000u) : (ktw[e >> 1] << 16));
-          fb[e] *= __uint_as_float((e & 1) ? (ksw[e >> 1] & 0xFFFF0000u) : (ksw[e >> 1] << 16));
-        }
-        bf16x8 ah, al, bh, bl;
-        split8(fa, ah, al);
-        split8(fb, bh, bl);
-        if (kk & 1) acc2 = mma3(ah, al, bh, bl, acc2);
-        else acc = mma3(ah, al, bh, bl, acc);
-      }
-      acc += acc2;
+      f32x4 run = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int t = 16 * ti + 4 * q + i;
-        sA[t * C + sr] = (ti == si && sr >= t) ? 0.f : sBeta[t] * acc[i];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) run[j] += fmaxf(graw[i][j], kGateFloor) * kLog2e;
+        Gl[i] = run;
+      }
+      // Sums of the earlier token groups: within a lane quad from its four values (added
+      // in one order on every lane), across the two quads of a group by row shifts of 4.
+      const int oq = og & 3;
+      const bool upper = og >= 4;
+      f32x4 base;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float q0 = quad_lane<0>(run[j]), q1 = quad_lane<1>(run[j]);
+        const float q2 = quad_lane<2>(run[j]), q3 = quad_lane<3>(run[j]);
+        const float e2 = q0 + q1, e3 = e2 + q2, tq = e3 + q3;
+        const float below = row_shr<4>(tq), above = row_shl<4>(tq);
+        const float eq = oq == 0 ? 0.f : oq == 1 ? q0 : oq == 2 ? e2 : e3;
+        const float ta = upper ? below : tq, tb = upper ? tq : above;
+        base[j] = upper ? ta + eq : eq;
+        gc[j] = ta + tb;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Gl[i] += base;
+    }
+    if (tid < C) sBeta[tid] = braw;
+    if (og == 7) {
+      f32x4 gam;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) gam[j] = ex2(gc[j]);
+      *reinterpret_cast<f32x4*>(sGam + c4) = gam;
+    }
+    {
+      const int wave_fast = __all(gc[0] >= -kFastRange && gc[1] >= -kFastRange &&
+                                  gc[2] >= -kFastRange && gc[3] >= -kFastRange);
+      if (lane == 0) sFast[w] = wave_fast;
+    }
+    __syncthreads();
+    const int4 fl = *reinterpret_cast<const int4*>(sFast);
+    const bool fast = fl.x && fl.y && fl.z && fl.w;
+
+    if (fast) {
+      // ---- fast path: K_G = k 2^G and Q = k 2^{-G} (rows = tokens), K_H^T = (k 2^{G_C - G})^T,
+      // split hi/lo, straight from this thread's registers.  Q takes the gate buffer, which
+      // the fast path does not use.
+      float kf[4][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        kf[i][0] = __uint_as_float(kq[i].x << 16);
+        kf[i][1] = __uint_as_float(kq[i].x & 0xFFFF0000u);
+        kf[i][2] = __uint_as_float(kq[i].y << 16);
+        kf[i][3] = __uint_as_float(kq[i].y & 0xFFFF0000u);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int o = (t4 + i) * SK + c4;
+        uint2 hi, lo;
+        split2(kf[i][0] * ex2(Gl[i][0]), kf[i][1] * ex2(Gl[i][1]), hi.x, lo.x);
+        split2(kf[i][2] * ex2(Gl[i][2]), kf[i][3] * ex2(Gl[i][3]), hi.y, lo.y);
+        *reinterpret_cast<uint2*>(sKGH + o) = hi;
+        *reinterpret_cast<uint2*>(sKGL + o) = lo;
+        split2(kf[i][0] * ex2(-Gl[i][0]), kf[i][1] * ex2(-Gl[i][1]), hi.x, lo.x);
+        split2(kf[i][2] * ex2(-Gl[i][2]), kf[i][3] * ex2(-Gl[i][3]), hi.y, lo.y);
+        *reinterpret_cast<uint2*>(sQH + o) = hi;
+        *reinterpret_cast<uint2*>(sQL + o) = lo;
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {   // K_H^T row c4 + j, tokens t4 .. t4 + 3
+        uint2 hi, lo;
+        split2(kf[0][j] * ex2(gc[j] - Gl[0][j]), kf[1][j] * ex2(gc[j] - Gl[1][j]), hi.x, lo.x);
+        split2(kf[2][j] * ex2(gc[j] - Gl[2][j]), kf[3][j] * ex2(gc[j] - Gl[3][j]), hi.y, lo.y);
+        *reinterpret_cast<uint2*>(sKHH + (c4 + j) * SV + t4) = hi;
+        *reinterpret_cast<uint2*>(sKHL + (c4 + j) * SV + t4) = lo;
+      }
+      __syncthreads();
+
+      // ---- A = Diag(beta) (strictly lower part of K_G Q^T), three 16x16 tiles ---------
+      if (w < 3) {
+        const int ti = w == 0 ? 0 : 1, si = w == 2 ? 1 : 0;
+        const int tr = 16 * ti + r, sr = 16 * si + r;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const int ot = tr * SK + 32 * kk + 4 * q, os = sr * SK + 32 * kk + 4 * q;
+          const bf16x8 ah = ld_op(sKGH + ot), al = ld_op(sKGL + ot);
+          const bf16x8 bh = ld_op(sQH + os), bl = ld_op(sQL + os);
+          if (kk & 1) acc2 = mma3(ah, al, bh, bl, acc2);
+          else acc = mma3(ah, al, bh, bl, acc);
+        }
+        acc += acc2;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t = 16 * ti + 4 * q + i;
+          sA[t * C + sr] = (ti == si && sr >= t) ? 0.f : sBeta[t] * acc[i];
+        }
       }
     } else {
-      // meanwhile wave 3: K_H^T = (k exp(G_C - G))^T, rows = channels, split hi/lo
+      // ---- strong-decay path ------------------------------------------------------------
+      // the running decays and keys into LDS, row-major
 #pragma unroll
-      for (int x = 0; x < 2; ++x) {
-        const int c = lane + 64 * x;
-        const float gC = sG[31 * SG + c];
+      for (int i = 0; i < 4; ++i) {
+        *reinterpret_cast<f32x4*>(sG + (t4 + i) * SG + c4) = Gl[i];
+        *reinterpret_cast<uint2*>(sK + (t4 + i) * SK + c4) = kq[i];
+      }
+      __syncthreads();
+      // A = Diag(beta) (strictly lower part of R Q^T), three 16x16 tiles on bf16 MFMA
+      // (16x16x32) with hi/lo split factors, like the state products: lane (q, r) feeds
+      // channels 32 kk + 8 q + e of its row to step kk (three MFMAs a step where fp32 MFMA
+      // would take eight, at a sixteenth of the bf16 rate).  Each tile factors the decay
+      // at its own reference token, so no factor exceeds 2^{8 |g|max}.
+      if (w < 3) {
+        const int ti = w == 0 ? 0 : 1, si = w == 2 ? 1 : 0;
+        const int rf = w == 0 ? 8 : (w == 1 ? 15 : 24);   // reference token of the tile
+        const int tr = 16 * ti + r, sr = 16 * si + r;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          float x[8];
+        for (int kk = 0; kk < 4; ++kk) {
+          const int c0 = 32 * kk + 8 * q;
+          float fa[8], fb[8];
+#pragma unroll
+          for (int h2 = 0; h2 < 2; ++h2) {
+            const f32x4 gt = *reinterpret_cast<const f32x4*>(sG + tr * SG + c0 + 4 * h2);
+            const f32x4 gs = *reinterpret_cast<const f32x4*>(sG + sr * SG + c0 + 4 * h2);
+            const f32x4 gf = *reinterpret_cast<const f32x4*>(sG + rf * SG + c0 + 4 * h2);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              fa[4 * h2 + i] = ex2(gt[i] - gf[i]);
+              fb[4 * h2 + i] = ex2(gf[i] - gs[i]);
+            }
+          }
+          const uint4 kt = *reinterpret_cast<const uint4*>(sK + tr * SK + c0);
+          const uint4 ks = *reinterpret_cast<const uint4*>(sK + sr * SK + c0);
+          const uint32_t ktw[4] = {kt.x, kt.y, kt.z, kt.w}, ksw[4] = {ks.x, ks.y, ks.z, ks.w};
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const int t = 8 * m + e;
-            x[e] = bf2f(sK[t * SK + c]) * ex2(gC - sG[t * SG + c]);
+            fa[e] *= __uint_as_float((e & 1) ? (ktw[e >> 1] & 0xFFFF0000u) : (ktw[e >> 1] << 16));
+            fb[e] *= __uint_as_float((e & 1) ? (ksw[e >> 1] & 0xFFFF0000u) : (ksw[e >> 1] << 16));
           }
-          bf16x8 hh, hl;
-          split8(x, hh, hl);
-          *reinterpret_cast<bf16x8*>(sKHH + c * SV + 8 * m) = hh;
-          *reinterpret_cast<bf16x8*>(sKHL + c * SV + 8 * m) = hl;
+          bf16x8 ah, al, bh, bl;
+          split8(fa, ah, al);
+          split8(fb, bh, bl);
+          if (kk & 1) acc2 = mma3(ah, al, bh, bl, acc2);
+          else acc = mma3(ah, al, bh, bl, acc);
         }
+        acc += acc2;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t = 16 * ti + 4 * q + i;
+          sA[t * C + sr] = (ti == si && sr >= t) ? 0.f : sBeta[t] * acc[i];
+        }
+      } else {
+        // meanwhile wave 3: K_H^T = (k exp(G_C - G))^T, rows = channels, split hi/lo
+#pragma unroll
+        for (int x = 0; x < 2; ++x) {
+          const int c = lane + 64 * x;
+          const float gC = sG[31 * SG + c];
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int t = 8 * m + e;
+              x[e] = bf2f(sK[t * SK + c]) * ex2(gC - sG[t * SG + c]);
+            }
+            bf16x8 hh, hl;
+            split8(x, hh, hl);
+            *reinterpret_cast<bf16x8*>(sKHH + c * SV + 8 * m) = hh;
+            *reinterpret_cast<bf16x8*>(sKHL + c * SV + 8 * m) = hl;
+          }
+        }
+      }
+      // K_G = k exp(G), rows = tokens: two (token, 8-channel) units per thread (the keys
+      // and gates are read here, before the substitution reuses the key buffer for T)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
+        const uint4 kr = *reinterpret_cast<const uint4*>(sK + t * SK + c8);
+        const uint32_t kw[4] = {kr.x, kr.y, kr.z, kr.w};
+        const f32x4 g0 = *reinterpret_cast<const f32x4*>(sG + t * SG + c8);
+        const f32x4 g1 = *reinterpret_cast<const f32x4*>(sG + t * SG + c8 + 4);
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float kv = __uint_as_float((e & 1) ? (kw[e >> 1] & 0xFFFF0000u) : (kw[e >> 1] << 16));
+          x[e] = kv * ex2(e < 4 ? g0[e & 3] : g1[e & 3]);
+        }
+        bf16x8 hh, hl;
+        split8(x, hh, hl);
+        *reinterpret_cast<bf16x8*>(sKGH + t * SK + c8) = hh;
+        *reinterpret_cast<bf16x8*>(sKGL + t * SK + c8) = hl;
       }
     }
     __syncthreads();
 
-    // ---- T = (I + A)^{-1}: diagonal 16x16 blocks by forward substitution -----------
-    if (w == 0 && lane < 32) {
-      const int base = 16 * (lane >> 4), s = lane & 15;
-      float x[16];
+    // ---- T = (I + A)^{-1}: diagonal 16x16 blocks on fp32 MFMA --------------------------
+    // A strictly lower 16x16 block B has B^16 = 0, so (I + B)^{-1} = (I - B)(I + B^2)(I + B^4)
+    // (I + B^8) exactly: six chained 16x16x16 products (four 16x16x4 MFMAs each) instead of
+    // a 16-step substitution.  Each power and its transpose are carried in the accumulator
+    // layout (lane (q, r) holds rows 4q + i of column r); the transpose supplies the left
+    // operand (its register i is the left factor's entry at row r, contraction index 4q + i)
+    // and the power itself the right operand, so the chain never leaves registers.
+    // Wave 0 inverts the block of tokens 0..15, wave 1 that of tokens 16..31.
+    if (w < 2) {
+      const int base = 16 * w;
+      f32x4 a, at;
 #pragma unroll
-      for (int t = 0; t < 16; ++t) {
-        float acc = (t == s) ? 1.f : 0.f;
-#pragma unroll
-        for (int rr = 0; rr < t; ++rr) acc = fmaf(-sA[(base + t) * C + base + rr], x[rr], acc);
-        x[t] = acc;
-        sT[(base + t) * C + base + s] = acc;
+      for (int i = 0; i < 4; ++i) {
+        a[i] = sA[(base + 4 * q + i) * C + base + r];
+        at[i] = sA[(base + r) * C + base + 4 * q + i];
       }
-    }
-    // K_G = k exp(G), rows = tokens: this thread's two (token, 8-channel) units, whose
-    // keys it still holds from the load
+      auto mul = [](const f32x4 left_t, const f32x4 right, f32x4 c) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
-      const uint32_t kw[4] = {kraw[u].x, kraw[u].y, kraw[u].z, kraw[u].w};
-      const f32x4 g0 = *reinterpret_cast<const f32x4*>(sG + t * SG + c8);
-      const f32x4 g1 = *reinterpret_cast<const f32x4*>(sG + t * SG + c8 + 4);
-      float x[8];
+        for (int i = 0; i < 4; ++i) c = mma32(left_t[i], right[i], c);
+        return c;
+      };
+      const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+      const f32x4 p2 = mul(at, a, zero), p2t = mul(a, at, zero);
+      const f32x4 p4 = mul(p2t, p2, zero), p4t = mul(p2, p2t, zero);
+      f32x4 rr = mul(p4t, p4, zero);                      // B^8
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float kv = __uint_as_float((e & 1) ? (kw[e >> 1] & 0xFFFF0000u) : (kw[e >> 1] << 16));
-        x[e] = kv * ex2(e < 4 ? g0[e & 3] : g1[e & 3]);
-      }
-      bf16x8 hh, hl;
-      split8(x, hh, hl);
-      *reinterpret_cast<bf16x8*>(sKGH + t * SK + c8) = hh;
-      *reinterpret_cast<bf16x8*>(sKGL + t * SK + c8) = hl;
+      for (int i = 0; i < 4; ++i) rr[i] += (4 * q + i == r) ? 1.f : 0.f;   // I + B^8
+      rr = mul(p4t, rr, rr);                              // (I + B^4)(I + B^8)
+      rr = mul(p2t, rr, rr);                              // (I + B^2) ...
+      rr = mul(-at, rr, rr);                              // (I - B) ...
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sT[(base + 4 * q + i) * C + base + r] = rr[i];
     }
+    // X = K_G S' (K_G is in LDS on both paths)
+    x_phase();
     // the next chunk's inputs load while this chunk finishes
     fetch(t0 + C);   // past the window this reads zeros
     __syncthreads();
@@ -388,38 +541,11 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         const int e = lt + 192 * u;
         const int t = e < 512 ? e >> 5 : 16 + ((e - 512) >> 4);
         const int s = e < 512 ? e & 31 : 16 + ((e - 512) & 15);
-        {
-          const float val = s <= t ? sT[t * C + s] * sBeta[s] : 0.f;
-          __bf16 a, b;
-          split(-val, a, b);
-          sTPH[t * SP + s] = a;
-          sTPL[t * SP + s] = b;
-        }
-      }
-    }
-    // (no barrier: X below reads only K_G and this wave's registers)
-
-    // ---- X = K_G S' on this wave's columns (rows t, contraction over channels) -------
-    f32x4 X[2][2] = {};
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      bf16x8 sh[2], slo[2];
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        float x[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = S[2 * kk + (e >> 2)][nt][e & 3];
-        split8(x, sh[nt], slo[nt]);
-      }
-#pragma unroll
-      for (int mu = 0; mu < 2; ++mu) {
-        const int o = (16 * mu + r) * SK + 32 * kk + 4 * q;
-        const bf16x8 ah = cat(*reinterpret_cast<const bf16x4*>(sKGH + o),
-                              *reinterpret_cast<const bf16x4*>(sKGH + o + 16));
-        const bf16x8 al = cat(*reinterpret_cast<const bf16x4*>(sKGL + o),
-                              *reinterpret_cast<const bf16x4*>(sKGL + o + 16));
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) X[mu][nt] = mma3(ah, al, sh[nt], slo[nt], X[mu][nt]);
+        const float val = s <= t ? sT[t * C + s] * sBeta[s] : 0.f;
+        __bf16 a, b;
+        split(-val, a, b);
+        sTPH[t * SP + s] = a;
+        sTPL[t * SP + s] = b;
       }
     }
 

@@ -26,6 +26,33 @@ __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* p, int bytes) {
 __device__ inline float ldf(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }
+__device__ inline f32x2 ldf2(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(f32x2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+}
+
+__device__ inline f32x4 ldf4(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// The value of the lane N places below (DPP row_shr:N) or above (row_shl:N) this one
+// within its row of 16 lanes; 0 where that lane is outside the row.
+template <int N>
+__device__ inline float row_shr(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                               0x110 + N, 0xF, 0xF, true));
+}
+template <int N>
+__device__ inline float row_shl(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                               0x100 + N, 0xF, 0xF, true));
+}
+
+// The value of lane L of this lane's group of four (DPP quad permute).
+template <int L>
+__device__ inline float quad_lane(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
+                                                               L * 0x55, 0xF, 0xF, false));
+}
 
 // p.x * m.x + p.y * m.y + c on the packed-bf16 dot product (v_dot2c_f32_bf16).  With m
 // a unit selector (+-1 in one half, 0 in the other) it reads one bf16 of a packed word
@@ -62,6 +89,15 @@ __device__ inline void split8(const float* x, bf16x8& hi, bf16x8& lo) {
   }
   hi = __builtin_bit_cast(bf16x8, make_uint4(h[0], h[1], h[2], h[3]));
   lo = __builtin_bit_cast(bf16x8, make_uint4(l[0], l[1], l[2], l[3]));
+}
+
+// Two values split at once into packed bf16 words: hi = (bf16(x0), bf16(x1)), lo = the
+// remainders (x - hi, exact in fp32) rounded to bf16, as in split8.
+__device__ inline void split2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  const bf16x2 hw = __builtin_convertvector(f32x2{x0, x1}, bf16x2);
+  const float r0 = dot2(hw, kNegLo, x0), r1 = dot2(hw, kNegHi, x1);
+  hi = __builtin_bit_cast(uint32_t, hw);
+  lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{r0, r1}, bf16x2));
 }
 
 __device__ inline f32x4 mma(bf16x8 a, bf16x8 b, f32x4 c) {
