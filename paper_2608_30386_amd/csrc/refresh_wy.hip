@@ -81,26 +81,28 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr int SG = 132;     // f32 [C][SG]   cumulative log2-decay
 constexpr int SK = 136;     // bf16 [C][SK]  keys, K_G
 constexpr int SV = 40;      // bf16 [D][SV]  K_H^T
-constexpr int SP = 36;      // bf16 [C][SP]  T' (8-byte aligned rows)
+constexpr int SP = 36;      // bf16 [C][SP]  diagonal blocks of T' (8-byte aligned rows)
+constexpr int ST = 36;      // f32  [C][ST]  A, then the diagonal blocks of T
 
-// LDS map (bytes).  The key buffer is dead once A and K_H are built and then holds
-// T and T'.  On the fast path the gate buffer holds Q (hi, lo) instead.
+// LDS map (bytes).  The key buffer is dead once A and K_H are built and then holds the
+// diagonal blocks of T'.  On the fast path the gate buffer holds Q (hi, lo) instead.
+// The A buffer keeps block (1, 0) of A; each diagonal block of A is replaced by the same
+// block of T.
 constexpr int G_BYTES = C * SG * 4 > 2 * C * SK * 2 ? C * SG * 4 : 2 * C * SK * 2;
 constexpr int OFF_G = 0;                       // f32  [C][SG]; fast path: bf16 [2][C][SK] Q
-constexpr int OFF_K = OFF_G + G_BYTES;         // bf16 [C][SK]  -> later T, T'
-constexpr int OFF_T = OFF_K;                   // f32  [C][C]
-constexpr int OFF_TPH = OFF_K + C * C * 4;     // bf16 [C][SP]
+constexpr int OFF_K = OFF_G + G_BYTES;         // bf16 [C][SK]  -> later T' diagonal blocks
+constexpr int OFF_TPH = OFF_K;                 // bf16 [C][SP]
 constexpr int OFF_TPL = OFF_TPH + C * SP * 2;
 constexpr int OFF_KGH = OFF_K + C * SK * 2;    // bf16 [C][SK]
 constexpr int OFF_KGL = OFF_KGH + C * SK * 2;
 constexpr int OFF_KHH = OFF_KGL + C * SK * 2;  // bf16 [D][SV]
 constexpr int OFF_KHL = OFF_KHH + D * SV * 2;
-constexpr int OFF_A = OFF_KHL + D * SV * 2;    // f32  [C][C]
-constexpr int OFF_BETA = OFF_A + C * C * 4;    // f32  [C]
+constexpr int OFF_A = OFF_KHL + D * SV * 2;    // f32  [C][ST]
+constexpr int OFF_BETA = OFF_A + C * ST * 4;   // f32  [C]
 constexpr int OFF_GAM = OFF_BETA + C * 4;      // f32  [D] exp(G_C)
 constexpr int OFF_FLAGS = OFF_GAM + D * 4;     // int  [4] per wave: fast path possible
 constexpr int LDS_BYTES = OFF_FLAGS + 4 * 4;
-static_assert(C * C * 4 + 2 * C * SP * 2 <= C * SK * 2, "T and T' must fit in the key buffer");
+static_assert(2 * C * SP * 2 <= C * SK * 2, "T' must fit in the key buffer");
 static_assert(LDS_BYTES <= 81920, "two blocks per CU");
 
 __device__ inline float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
@@ -117,7 +119,6 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDS_BYTES];
   float* sG = reinterpret_cast<float*>(smem + OFF_G);
   uint16_t* sK = reinterpret_cast<uint16_t*>(smem + OFF_K);
-  float* sT = reinterpret_cast<float*>(smem + OFF_T);
   __bf16* sKGH = reinterpret_cast<__bf16*>(smem + OFF_KGH);
   __bf16* sKGL = reinterpret_cast<__bf16*>(smem + OFF_KGL);
   __bf16* sKHH = reinterpret_cast<__bf16*>(smem + OFF_KHH);
@@ -156,7 +157,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   // free until the first chunk.
   using dasc::kOmitted;
   int64_t* sOff = reinterpret_cast<int64_t*>(smem + OFF_A);
-  static_assert(D * 8 <= C * C * 4, "row table must fit in the A buffer");
+  static_assert(D * 8 <= C * ST * 4, "row table must fit in the A buffer");
   if (FUSED) {
     if (tid < D) sOff[tid] = dasc::ckpt_row_offset(inv_row[head_row + tid], ck, cslot, D);
     __syncthreads();
@@ -245,32 +246,42 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         vreg[mu][i] = __builtin_amdgcn_raw_buffer_load_b32(
             rv, ((16 * mu + 4 * q + i) * D + 32 * w + 2 * r) * 2, c0 * D * 2, 0);
   };
-  // X = K_G S' on this wave's columns (rows t, contraction over channels)
+  // X = K_G S' on this wave's columns (rows t, contraction over channels), one step per
+  // 32 channels
   f32x4 X[2][2];
-  auto x_phase = [&]() {
+  auto x_step = [&](int kk) {
+    bf16x8 sh[2], slo[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = S[2 * kk + (e >> 2)][nt][e & 3];
+      split8(x, sh[nt], slo[nt]);
+    }
+#pragma unroll
+    for (int mu = 0; mu < 2; ++mu) {
+      const int o = (16 * mu + r) * SK + 32 * kk + 4 * q;
+      const bf16x8 ah = ld_op(sKGH + o), al = ld_op(sKGL + o);
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) X[mu][nt] = mma3(ah, al, sh[nt], slo[nt], X[mu][nt]);
+    }
+  };
+  auto x_init = [&]() {
 #pragma unroll
     for (int mu = 0; mu < 2; ++mu)
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) X[mu][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      bf16x8 sh[2], slo[2];
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        float x[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = S[2 * kk + (e >> 2)][nt][e & 3];
-        split8(x, sh[nt], slo[nt]);
-      }
-#pragma unroll
-      for (int mu = 0; mu < 2; ++mu) {
-        const int o = (16 * mu + r) * SK + 32 * kk + 4 * q;
-        const bf16x8 ah = ld_op(sKGH + o), al = ld_op(sKGL + o);
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) X[mu][nt] = mma3(ah, al, sh[nt], slo[nt], X[mu][nt]);
-      }
-    }
   };
+  // left * right on fp32 MFMA (16x16x4, four steps) for 16x16 blocks in the accumulator
+  // layout (lane (q, r) holds rows 4q + i of column r): the right factor as it is, the left
+  // one as its transpose (register i of lane (q, r) is then the left factor's entry at row r,
+  // contraction index 4q + i), so products chain without leaving registers.
+  auto mul = [](const f32x4 left_t, const f32x4 right, f32x4 c) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) c = mma32(left_t[i], right[i], c);
+    return c;
+  };
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
   fetch(0);
   fetch_v(0);
 
@@ -306,12 +317,10 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       for (int i = 0; i < 4; ++i) Gl[i] += base;
     }
     if (tid < C) sBeta[tid] = braw;
-    if (og == 7) {
-      f32x4 gam;
+    f32x4 gam;   // 2^{G_C} on channels c4 .. c4 + 3
 #pragma unroll
-      for (int j = 0; j < 4; ++j) gam[j] = ex2(gc[j]);
-      *reinterpret_cast<f32x4*>(sGam + c4) = gam;
-    }
+    for (int j = 0; j < 4; ++j) gam[j] = ex2(gc[j]);
+    if (og == 7) *reinterpret_cast<f32x4*>(sGam + c4) = gam;
     {
       const int wave_fast = __all(gc[0] >= -kFastRange && gc[1] >= -kFastRange &&
                                   gc[2] >= -kFastRange && gc[3] >= -kFastRange);
@@ -321,8 +330,11 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     const int4 fl = *reinterpret_cast<const int4*>(sFast);
     const bool fast = fl.x && fl.y && fl.z && fl.w;
 
+    // Waves 0 and 2 hold diagonal block w / 2 of A and its transpose in the accumulator
+    // layout (a, at); wave 1 leaves block (1, 0) of A in the A buffer.
+    f32x4 a = zero4, at = zero4;
     if (fast) {
-      // ---- fast path: K_G = k 2^G and Q = k 2^{-G} (rows = tokens), K_H^T = (k 2^{G_C - G})^T,
+      // ---- fast path: K_G = k 2^G and Q = k 2^{-G} (rows = tokens), K_H^T = (Q 2^{G_C})^T,
       // split hi/lo, straight from this thread's registers.  Q takes the gate buffer, which
       // the fast path does not use.
       float kf[4][4];
@@ -333,34 +345,44 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         kf[i][2] = __uint_as_float(kq[i].y << 16);
         kf[i][3] = __uint_as_float(kq[i].y & 0xFFFF0000u);
       }
+      float qf[4][4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int o = (t4 + i) * SK + c4;
+        float kg[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          kg[j] = kf[i][j] * ex2(Gl[i][j]);
+          qf[i][j] = kf[i][j] * ex2(-Gl[i][j]);
+        }
         uint2 hi, lo;
-        split2(kf[i][0] * ex2(Gl[i][0]), kf[i][1] * ex2(Gl[i][1]), hi.x, lo.x);
-        split2(kf[i][2] * ex2(Gl[i][2]), kf[i][3] * ex2(Gl[i][3]), hi.y, lo.y);
+        split2(kg[0], kg[1], hi.x, lo.x);
+        split2(kg[2], kg[3], hi.y, lo.y);
         *reinterpret_cast<uint2*>(sKGH + o) = hi;
         *reinterpret_cast<uint2*>(sKGL + o) = lo;
-        split2(kf[i][0] * ex2(-Gl[i][0]), kf[i][1] * ex2(-Gl[i][1]), hi.x, lo.x);
-        split2(kf[i][2] * ex2(-Gl[i][2]), kf[i][3] * ex2(-Gl[i][3]), hi.y, lo.y);
+        split2(qf[i][0], qf[i][1], hi.x, lo.x);
+        split2(qf[i][2], qf[i][3], hi.y, lo.y);
         *reinterpret_cast<uint2*>(sQH + o) = hi;
         *reinterpret_cast<uint2*>(sQL + o) = lo;
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {   // K_H^T row c4 + j, tokens t4 .. t4 + 3
         uint2 hi, lo;
-        split2(kf[0][j] * ex2(gc[j] - Gl[0][j]), kf[1][j] * ex2(gc[j] - Gl[1][j]), hi.x, lo.x);
-        split2(kf[2][j] * ex2(gc[j] - Gl[2][j]), kf[3][j] * ex2(gc[j] - Gl[3][j]), hi.y, lo.y);
+        split2(qf[0][j] * gam[j], qf[1][j] * gam[j], hi.x, lo.x);
+        split2(qf[2][j] * gam[j], qf[3][j] * gam[j], hi.y, lo.y);
         *reinterpret_cast<uint2*>(sKHH + (c4 + j) * SV + t4) = hi;
         *reinterpret_cast<uint2*>(sKHL + (c4 + j) * SV + t4) = lo;
       }
       __syncthreads();
 
-      // ---- A = Diag(beta) (strictly lower part of K_G Q^T), three 16x16 tiles ---------
+      // ---- A = Diag(beta) (strictly lower part of K_G Q^T): waves 0 and 2 a diagonal block
+      // and, from the same operands swapped, its transpose; wave 1 block (1, 0).
       if (w < 3) {
         const int ti = w == 0 ? 0 : 1, si = w == 2 ? 1 : 0;
         const int tr = 16 * ti + r, sr = 16 * si + r;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
+        const f32x4 bt = *reinterpret_cast<const f32x4*>(sBeta + 16 * ti + 4 * q);
+        const float bs = sBeta[tr];
+        f32x4 acc = zero4, acc2 = zero4, tacc = zero4, tacc2 = zero4;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
           const int ot = tr * SK + 32 * kk + 4 * q, os = sr * SK + 32 * kk + 4 * q;
@@ -368,12 +390,22 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
           const bf16x8 bh = ld_op(sQH + os), bl = ld_op(sQL + os);
           if (kk & 1) acc2 = mma3(ah, al, bh, bl, acc2);
           else acc = mma3(ah, al, bh, bl, acc);
+          if (w != 1) {
+            if (kk & 1) tacc2 = mma3(bh, bl, ah, al, tacc2);
+            else tacc = mma3(bh, bl, ah, al, tacc);
+          }
         }
         acc += acc2;
+        tacc += tacc2;
+        if (w == 1) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int t = 16 * ti + 4 * q + i;
-          sA[t * C + sr] = (ti == si && sr >= t) ? 0.f : sBeta[t] * acc[i];
+          for (int i = 0; i < 4; ++i) sA[(16 + 4 * q + i) * ST + r] = bt[i] * acc[i];
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            a[i] = r < 4 * q + i ? bt[i] * acc[i] : 0.f;    // A[base + 4q + i][base + r]
+            at[i] = 4 * q + i < r ? bs * tacc[i] : 0.f;     // A[base + r][base + 4q + i]
+          }
         }
       }
     } else {
@@ -394,7 +426,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         const int ti = w == 0 ? 0 : 1, si = w == 2 ? 1 : 0;
         const int rf = w == 0 ? 8 : (w == 1 ? 15 : 24);   // reference token of the tile
         const int tr = 16 * ti + r, sr = 16 * si + r;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
+        f32x4 acc = zero4, acc2 = zero4;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
           const int c0 = 32 * kk + 8 * q;
@@ -428,7 +460,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int t = 16 * ti + 4 * q + i;
-          sA[t * C + sr] = (ti == si && sr >= t) ? 0.f : sBeta[t] * acc[i];
+          sA[t * ST + sr] = (ti == si && sr >= t) ? 0.f : sBeta[t] * acc[i];
         }
       } else {
         // meanwhile wave 3: K_H^T = (k exp(G_C - G))^T, rows = channels, split hi/lo
@@ -452,7 +484,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         }
       }
       // K_G = k exp(G), rows = tokens: two (token, 8-channel) units per thread (the keys
-      // and gates are read here, before the substitution reuses the key buffer for T)
+      // and gates are read here, before T' reuses the key buffer)
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int t = (tid + 256 * u) >> 4, c8 = ((tid + 256 * u) & 15) * 8;
@@ -471,85 +503,75 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         *reinterpret_cast<bf16x8*>(sKGH + t * SK + c8) = hh;
         *reinterpret_cast<bf16x8*>(sKGL + t * SK + c8) = hl;
       }
+      __syncthreads();
+      if (w == 0 || w == 2) {
+        const int base = 8 * w;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          a[i] = sA[(base + 4 * q + i) * ST + base + r];
+          at[i] = sA[(base + r) * ST + base + 4 * q + i];
+        }
+      }
     }
-    __syncthreads();
 
-    // ---- T = (I + A)^{-1}: diagonal 16x16 blocks on fp32 MFMA --------------------------
-    // A strictly lower 16x16 block B has B^16 = 0, so (I + B)^{-1} = (I - B)(I + B^2)(I + B^4)
-    // (I + B^8) exactly: six chained 16x16x16 products (four 16x16x4 MFMAs each) instead of
-    // a 16-step substitution.  Each power and its transpose are carried in the accumulator
-    // layout (lane (q, r) holds rows 4q + i of column r); the transpose supplies the left
-    // operand (its register i is the left factor's entry at row r, contraction index 4q + i)
-    // and the power itself the right operand, so the chain never leaves registers.
-    // Wave 0 inverts the block of tokens 0..15, wave 1 that of tokens 16..31.
-    if (w < 2) {
-      const int base = 16 * w;
-      f32x4 a, at;
+    // ---- diagonal blocks of T = (I + A)^{-1} on fp32 MFMA, and X = K_G S' ---------------
+    // A strictly lower 16x16 block B has B^16 = 0, so (I + B)^{-1} = X1 X2 exactly with
+    // X1 = (I - B)(I + B^2) and X2 = (I + B^4)(I + B^8): eight chained 16x16x16 products
+    // (four 16x16x4 MFMAs each) in five dependent levels, each power carried together with
+    // its transpose.  Waves 0 and 2 invert their block with the steps of X in between (the
+    // two are independent, so the matrix pipe overlaps them); waves 1 and 3 only form X.
+    x_init();
+    if (w == 0 || w == 2) {
+      const int base = 8 * w;
+      f32x4 id;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) id[i] = 4 * q + i == r ? 1.f : 0.f;
+      const f32x4 imt = id - at;                           // (I - B)^T
+      const f32x4 p2 = mul(at, a, zero4);                  // B^2
+      const f32x4 p2t = mul(a, at, zero4);                 // (B^2)^T
+      x_step(0);
+      const f32x4 p4 = mul(p2t, p2, zero4);                // B^4
+      const f32x4 p4t = mul(p2, p2t, zero4);               // (B^4)^T
+      const f32x4 x1t = mul(p2, imt, imt);                 // X1^T = (I + B^2)^T (I - B)^T
+      x_step(1);
+      const f32x4 p8 = mul(p4t, p4, zero4) + id;           // I + B^8
+      x_step(2);
+      const f32x4 x2 = mul(p4t, p8, p8);                   // X2
+      x_step(3);
+      const f32x4 tb = mul(x1t, x2, zero4);                // T block: rows 4q + i, column r
+      const float bs = sBeta[base + r];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        a[i] = sA[(base + 4 * q + i) * C + base + r];
-        at[i] = sA[(base + r) * C + base + 4 * q + i];
+        const int t = base + 4 * q + i;
+        sA[t * ST + base + r] = tb[i];
+        __bf16 hi, lo;
+        split(-tb[i] * bs, hi, lo);   // -T' = -T Diag(beta)
+        sTPH[t * SP + base + r] = hi;
+        sTPL[t * SP + base + r] = lo;
       }
-      auto mul = [](const f32x4 left_t, const f32x4 right, f32x4 c) {
+    } else {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) c = mma32(left_t[i], right[i], c);
-        return c;
-      };
-      const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
-      const f32x4 p2 = mul(at, a, zero), p2t = mul(a, at, zero);
-      const f32x4 p4 = mul(p2t, p2, zero), p4t = mul(p2, p2t, zero);
-      f32x4 rr = mul(p4t, p4, zero);                      // B^8
-#pragma unroll
-      for (int i = 0; i < 4; ++i) rr[i] += (4 * q + i == r) ? 1.f : 0.f;   // I + B^8
-      rr = mul(p4t, rr, rr);                              // (I + B^4)(I + B^8)
-      rr = mul(p2t, rr, rr);                              // (I + B^2) ...
-      rr = mul(-at, rr, rr);                              // (I - B) ...
-#pragma unroll
-      for (int i = 0; i < 4; ++i) sT[(base + 4 * q + i) * C + base + r] = rr[i];
+      for (int kk = 0; kk < 4; ++kk) x_step(kk);
     }
-    // X = K_G S' (K_G is in LDS on both paths)
-    x_phase();
     // the next chunk's inputs load while this chunk finishes
     fetch(t0 + C);   // past the window this reads zeros
     __syncthreads();
-    // -T' = -T Diag(beta), split hi/lo (stored negated so that U takes X - V, which one
-    // dot2 per value forms from the packed values).  Wave 1 forms the off-diagonal block
-    // T10 = -T11 (A10 T00) on fp32 MFMA, the product staying in registers between the
-    // two steps; the other waves write the diagonal blocks and the zero upper block.
-    if (w == 1) {
-      f32x4 y = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        y = mma32(sA[(16 + r) * C + 4 * q + i], sT[(4 * q + i) * C + r], y);
-      f32x4 z = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) z = mma32(sT[(16 + r) * C + 16 + 4 * q + i], y[i], z);
-      const float br = sBeta[r];
+
+    // ---- block (1, 0) of -T' = -T Diag(beta): T10 = -T11 A10 T00, formed by every wave as
+    // its transpose T10^T = -T00^T (A10^T T11^T), which lands in the left-operand layout of
+    // the U product (lane (q, r) register i: row r, token 4q + i).
+    f32x4 tq;
+    {
+      f32x4 a10, t11t, t00;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int t = 16 + 4 * q + i;
-        __bf16 a, b;
-        split(z[i] * br, a, b);   // -T'10
-        sTPH[t * SP + r] = a;
-        sTPL[t * SP + r] = b;
+        a10[i] = sA[(16 + 4 * q + i) * ST + r];
+        t11t[i] = sA[(16 + r) * ST + 16 + 4 * q + i];
+        t00[i] = sA[(4 * q + i) * ST + r];
       }
-    } else {
-      const int lt = w == 0 ? tid : tid - 64;       // 0 .. 191
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        // 768 entries outside block (1,0): rows 0..15 whole, rows 16..31 columns 16..31
-        const int e = lt + 192 * u;
-        const int t = e < 512 ? e >> 5 : 16 + ((e - 512) >> 4);
-        const int s = e < 512 ? e & 31 : 16 + ((e - 512) & 15);
-        const float val = s <= t ? sT[t * C + s] * sBeta[s] : 0.f;
-        __bf16 a, b;
-        split(-val, a, b);
-        sTPH[t * SP + s] = a;
-        sTPL[t * SP + s] = b;
-      }
+      const f32x4 b4 = *reinterpret_cast<const f32x4*>(sBeta + 4 * q);
+      tq = mul(t00, mul(a10, t11t, zero4), zero4) * b4;
     }
-
-    __syncthreads();   // T' complete
 
     // ---- U = (-T')(X - V): the difference stays in registers as the B operand ------
     f32x4 U[2][2];
@@ -567,15 +589,20 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         split8(x, yh[nt], yl[nt]);
       }
       fetch_v(t0 + C);   // the next chunk's values (zeros past the window)
+      uint2 qh, ql;
+      split2(tq[0], tq[1], qh.x, ql.x);
+      split2(tq[2], tq[3], qh.y, ql.y);
+      const bf16x4 z4 = {};
+      // rows 0..15: (T'00, 0); rows 16..31: (T'10, T'11)
+      const int o0 = r * SP + 4 * q, o1 = (16 + r) * SP + 16 + 4 * q;
+      const bf16x8 ah0 = cat(*reinterpret_cast<const bf16x4*>(sTPH + o0), z4);
+      const bf16x8 al0 = cat(*reinterpret_cast<const bf16x4*>(sTPL + o0), z4);
+      const bf16x8 ah1 = cat(__builtin_bit_cast(bf16x4, qh), *reinterpret_cast<const bf16x4*>(sTPH + o1));
+      const bf16x8 al1 = cat(__builtin_bit_cast(bf16x4, ql), *reinterpret_cast<const bf16x4*>(sTPL + o1));
 #pragma unroll
-      for (int mu = 0; mu < 2; ++mu) {
-        const int o = (16 * mu + r) * SP + 4 * q;
-        const bf16x8 ah = cat(*reinterpret_cast<const bf16x4*>(sTPH + o),
-                              *reinterpret_cast<const bf16x4*>(sTPH + o + 16));
-        const bf16x8 al = cat(*reinterpret_cast<const bf16x4*>(sTPL + o),
-                              *reinterpret_cast<const bf16x4*>(sTPL + o + 16));
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) U[mu][nt] = mma3(ah, al, yh[nt], yl[nt], f32x4{0.f, 0.f, 0.f, 0.f});
+      for (int nt = 0; nt < 2; ++nt) {
+        U[0][nt] = mma3(ah0, al0, yh[nt], yl[nt], zero4);
+        U[1][nt] = mma3(ah1, al1, yh[nt], yl[nt], zero4);
       }
     }
 
