@@ -219,7 +219,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   f32x4 graw[4];
   uint2 kq[4];
   float braw;
-  auto fetch = [&](int c0) {
+  auto fetch_g = [&](int c0) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       if (PER_CHANNEL) {
@@ -228,10 +228,14 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         const float x = ldf(rg, (t4 + i) * 4, c0 * 4);
         graw[i] = f32x4{x, x, x, x};
       }
-      kq[i] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
-                                            rk, ((t4 + i) * D + c4) * 2, c0 * D * 2, 0));
     }
     braw = ldf(rb, (tid & (C - 1)) * 4, c0 * 4);
+  };
+  auto fetch_k = [&](int c0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      kq[i] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
+                                            rk, ((t4 + i) * D + c4) * 2, c0 * D * 2, 0));
   };
   // Values stay in registers in the layout the U phase consumes: lane (q, r) of wave w
   // holds, for tokens 16 mu + 4q + i, the word with columns 32w + 2r (low half) and
@@ -282,10 +286,27 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     return c;
   };
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
-  fetch(0);
+  // Issued in the order the loop issues them (gates, keys, values), so that the wait for
+  // a chunk's gates at the top of the loop is the same count on entry as on the back edge
+  // and does not also wait for the values.
+  __builtin_amdgcn_sched_barrier(0);
+  fetch_g(0);
+  __builtin_amdgcn_sched_barrier(0);
+  fetch_k(0);
+  __builtin_amdgcn_sched_barrier(0);
   fetch_v(0);
+  __builtin_amdgcn_sched_barrier(0);
 
+  // Two blocks share a CU, and the instruction arbiter prefers the older block's waves: left
+  // alone, the block placed first runs its chunks ~1.5x as fast as the other, which then
+  // finishes alone.  The later half of the grid (placed second) takes the higher wave
+  // priority for its first 60% of chunks, the earlier half for the rest, so that the pair
+  // finishes at about the same time.
+  const bool second = blockIdx.x >= (gridDim.x + 1) / 2;
+  const int t_flip = ((W + C - 1) / C * 3 / 5) * C;
   for (int t0 = 0; t0 < W; t0 += C) {
+    if ((t0 < t_flip) == second) __builtin_amdgcn_s_setprio(1);
+    else __builtin_amdgcn_s_setprio(0);
     // ---- stage the prefetched gates (running sums) and beta ------------------------------
     f32x4 Gl[4];   // G at tokens t4 + i, channels c4 .. c4 + 3
     f32x4 gc;      // G at the chunk's last token
@@ -317,6 +338,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       for (int i = 0; i < 4; ++i) Gl[i] += base;
     }
     if (tid < C) sBeta[tid] = braw;
+    fetch_g(t0 + C);   // the next chunk's gates (zeros past the window)
     f32x4 gam;   // 2^{G_C} on channels c4 .. c4 + 3
 #pragma unroll
     for (int j = 0; j < 4; ++j) gam[j] = ex2(gc[j]);
@@ -520,6 +542,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     // (four 16x16x4 MFMAs each) in five dependent levels, each power carried together with
     // its transpose.  Waves 0 and 2 invert their block with the steps of X in between (the
     // two are independent, so the matrix pipe overlaps them); waves 1 and 3 only form X.
+    fetch_k(t0 + C);   // the next chunk's keys
     x_init();
     if (w == 0 || w == 2) {
       const int base = 8 * w;
@@ -553,8 +576,6 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) x_step(kk);
     }
-    // the next chunk's inputs load while this chunk finishes
-    fetch(t0 + C);   // past the window this reads zeros
     __syncthreads();
 
     // ---- block (1, 0) of -T' = -T Diag(beta): T10 = -T11 A10 T00, formed by every wave as
