@@ -98,10 +98,13 @@ constexpr int OFF_KGL = OFF_KGH + C * SK * 2;
 constexpr int OFF_KHH = OFF_KGL + C * SK * 2;  // bf16 [D][SV]
 constexpr int OFF_KHL = OFF_KHH + D * SV * 2;
 constexpr int OFF_A = OFF_KHL + D * SV * 2;    // f32  [C][ST]
-constexpr int OFF_BETA = OFF_A + C * ST * 4;   // f32  [C]
-constexpr int OFF_GAM = OFF_BETA + C * 4;      // f32  [D] exp(G_C)
-constexpr int OFF_FLAGS = OFF_GAM + D * 4;     // int  [4] per wave: fast path possible
-constexpr int LDS_BYTES = OFF_FLAGS + 4 * 4;
+// Per-chunk scalars alternate between two copies by chunk parity, so that a chunk can
+// stage them while the waves still finishing the previous one read theirs.
+constexpr int OFF_BETA = OFF_A + C * ST * 4;   // f32  [2][C]
+constexpr int OFF_GAM = OFF_BETA + 2 * C * 4;  // f32  [2][D] exp(G_C)
+constexpr int OFF_FLAGS = OFF_GAM + 2 * D * 4; // int  [2][4] per wave: fast path possible
+constexpr int OFF_OMIT = OFF_FLAGS + 2 * 4 * 4;  // u8 [D] row omitted (replayed)
+constexpr int LDS_BYTES = OFF_OMIT + D;
 static_assert(2 * C * SP * 2 <= C * SK * 2, "T' must fit in the key buffer");
 static_assert(LDS_BYTES <= 81920, "two blocks per CU");
 
@@ -126,9 +129,10 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   float* sA = reinterpret_cast<float*>(smem + OFF_A);
   __bf16* sTPH = reinterpret_cast<__bf16*>(smem + OFF_TPH);
   __bf16* sTPL = reinterpret_cast<__bf16*>(smem + OFF_TPL);
-  float* sBeta = reinterpret_cast<float*>(smem + OFF_BETA);
-  float* sGam = reinterpret_cast<float*>(smem + OFF_GAM);
-  int* sFast = reinterpret_cast<int*>(smem + OFF_FLAGS);
+  float* const sBeta2 = reinterpret_cast<float*>(smem + OFF_BETA);
+  float* const sGam2 = reinterpret_cast<float*>(smem + OFF_GAM);
+  int* const sFast2 = reinterpret_cast<int*>(smem + OFF_FLAGS);
+  unsigned char* const sOmit = smem + OFF_OMIT;
   __bf16* sQH = reinterpret_cast<__bf16*>(smem + OFF_G);   // fast path only
   __bf16* sQL = sQH + C * SK;
 
@@ -140,7 +144,10 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 
   const int64_t head_row = (int64_t(layer) * H + h) * D;
   bool mine = false;
-  if (tid < D) mine = inv_row[head_row + tid] < 0;
+  if (tid < D) {
+    mine = inv_row[head_row + tid] < 0;
+    sOmit[tid] = mine;
+  }
   const bool any_omitted = __syncthreads_or(mine);
   if (!FUSED && !any_omitted) return;
   const int64_t sl = slot[n];
@@ -302,11 +309,15 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   // finishes alone.  The later half of the grid (placed second) takes the higher wave
   // priority for its first 60% of chunks, the earlier half for the rest, so that the pair
   // finishes at about the same time.
-  const bool second = blockIdx.x >= (gridDim.x + 1) / 2;
+  const int second = __builtin_amdgcn_readfirstlane(blockIdx.x >= (gridDim.x + 1) / 2 ? 1 : 0);
   const int t_flip = ((W + C - 1) / C * 3 / 5) * C;
   for (int t0 = 0; t0 < W; t0 += C) {
-    if ((t0 < t_flip) == second) __builtin_amdgcn_s_setprio(1);
+    if ((t0 < t_flip) == (second != 0)) __builtin_amdgcn_s_setprio(1);
     else __builtin_amdgcn_s_setprio(0);
+    const int par = (t0 / C) & 1;
+    float* const sBeta = sBeta2 + par * C;
+    float* const sGam = sGam2 + par * D;
+    int* const sFast = sFast2 + par * 4;
     // ---- stage the prefetched gates (running sums) and beta ------------------------------
     f32x4 Gl[4];   // G at tokens t4 + i, channels c4 .. c4 + 3
     f32x4 gc;      // G at the chunk's last token
@@ -318,21 +329,28 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         for (int j = 0; j < 4; ++j) run[j] += fmaxf(graw[i][j], kGateFloor) * kLog2e;
         Gl[i] = run;
       }
-      // Sums of the earlier token groups: within a lane quad from its four values (added
-      // in one order on every lane), across the two quads of a group by row shifts of 4.
-      const int oq = og & 3;
-      const bool upper = og >= 4;
-      f32x4 base;
+      // Sums of the earlier token groups (lanes 8 cq .. 8 cq + 7 hold the eight groups of a
+      // channel quad), without branches: within a lane quad, the values shifted up by one lane
+      // (zero into the first) are summed by two shift-and-add steps; the upper quad adds the
+      // lower quad's total (row shift of 4).  All eight lanes form the chunk total as
+      // (lower total) + (upper total).
+      // The selects are bitwise (all-ones / zero lane masks): a conditional expression lets
+      // the compiler move a DPP read under an exec mask, where a lane whose source lane is
+      // masked off reads a stale value.
+      const uint32_t m_first = (og & 3) == 0 ? ~0u : 0u, m_upper = og >= 4 ? ~0u : 0u;
+      f32x4 x, base;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) x[j] = bsel(m_first, 0.f, quad_perm<0x90>(run[j]));   // [0,0,1,2]
+#pragma unroll
+      for (int j = 0; j < 4; ++j) x[j] += quad_perm<0x90>(x[j]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) x[j] += quad_perm<0x40>(x[j]);                        // [0,0,0,1]
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float q0 = quad_lane<0>(run[j]), q1 = quad_lane<1>(run[j]);
-        const float q2 = quad_lane<2>(run[j]), q3 = quad_lane<3>(run[j]);
-        const float e2 = q0 + q1, e3 = e2 + q2, tq = e3 + q3;
+        const float tq = quad_perm<0xFF>(x[j] + run[j]);                                 // [3,3,3,3]
         const float below = row_shr<4>(tq), above = row_shl<4>(tq);
-        const float eq = oq == 0 ? 0.f : oq == 1 ? q0 : oq == 2 ? e2 : e3;
-        const float ta = upper ? below : tq, tb = upper ? tq : above;
-        base[j] = upper ? ta + eq : eq;
-        gc[j] = ta + tb;
+        base[j] = x[j] + bsel(m_upper, below, 0.f);
+        gc[j] = bsel(m_upper, below + tq, tq + above);
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) Gl[i] += base;
@@ -344,8 +362,8 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     for (int j = 0; j < 4; ++j) gam[j] = ex2(gc[j]);
     if (og == 7) *reinterpret_cast<f32x4*>(sGam + c4) = gam;
     {
-      const int wave_fast = __all(gc[0] >= -kFastRange && gc[1] >= -kFastRange &&
-                                  gc[2] >= -kFastRange && gc[3] >= -kFastRange);
+      const float gmin = fminf(fminf(gc[0], gc[1]), fminf(gc[2], gc[3]));
+      const int wave_fast = __all(gmin >= -kFastRange);
       if (lane == 0) sFast[w] = wave_fast;
     }
     __syncthreads();
@@ -647,21 +665,23 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) S[mt][nt] = mma3(ah, al, uh[nt], ul[nt], S[mt][nt] * gam);
     }
-    __syncthreads();
+    // (no barrier: the next chunk stages into the other copy of the per-chunk scalars, and
+    // writes the factor buffers read here only after its first barrier)
   }
 
 #pragma unroll
-  for (int mt = 0; mt < 8; ++mt)
+  for (int mt = 0; mt < 8; ++mt) {
+    // rows 16 mt + 4q .. 16 mt + 4q + 3: one omitted flag per byte
+    const uint32_t om = *reinterpret_cast<const uint32_t*>(sOmit + 16 * mt + 4 * q);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int c = 16 * mt + 4 * q + i;
-      // re-read (volatile): merged with the loads of the start, 32 predicates would stay
-      // live through the replay and spill
-      if (reinterpret_cast<const volatile int32_t*>(inv_row)[head_row + c] < 0) {
+      if ((om >> (8 * i)) & 0xFFu) {
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) S_head[int64_t(c) * D + 32 * w + 2 * r + nt] = S[mt][nt][i];
       }
     }
+  }
 }
 
 }  // namespace

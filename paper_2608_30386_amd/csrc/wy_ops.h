@@ -47,11 +47,18 @@ __device__ inline float row_shl(float v) {
                                                                0x100 + N, 0xF, 0xF, true));
 }
 
-// The value of lane L of this lane's group of four (DPP quad permute).
-template <int L>
-__device__ inline float quad_lane(float v) {
+// (m & a) | (~m & b) on the bits: with m all ones or all zeros per lane, a select that
+// stays a single v_bfi_b32 on every lane.
+__device__ inline float bsel(uint32_t m, float a, float b) {
+  return __uint_as_float((__float_as_uint(a) & m) | (__float_as_uint(b) & ~m));
+}
+
+// DPP quad permute: lane k of each group of four takes the value of lane (CTRL >> 2k) & 3
+// of its group (0x55 L broadcasts lane L; 0x90 = [0,0,1,2] shifts up by one lane).
+template <int CTRL>
+__device__ inline float quad_perm(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v),
-                                                               L * 0x55, 0xF, 0xF, false));
+                                                               CTRL, 0xF, 0xF, false));
 }
 
 // p.x * m.x + p.y * m.y + c on the packed-bf16 dot product (v_dot2c_f32_bf16).  With m
