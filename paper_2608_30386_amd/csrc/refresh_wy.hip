@@ -16,11 +16,12 @@
 // K_H, A, T') is built cooperatively in LDS each chunk; then each wave runs its three
 // chained contractions K_G S', T'(V - .), K_H^T U on its own columns.
 //
-// Precision.  Every product runs on v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
-// An fp32 operand x is split into x_hi = bf16(x) and x_lo = bf16(x - x_hi); a product
-// is formed as a_lo b_hi + a_hi b_lo + a_hi b_hi, which keeps ~16 mantissa bits per
-// term.  This is what lets an fp32 state survive thousands of tokens within 2e-3 while
-// running at the bf16 matrix-core rate.
+// Precision.  The products run on bf16 MFMA (16x16x32; 16x16x16 for the diagonal blocks
+// of T) with fp32 accumulation.  An fp32 operand x is split into x_hi = bf16(x) and
+// x_lo = bf16(x - x_hi); a product is formed as a_lo b_hi + a_hi b_lo + a_hi b_hi, which
+// keeps ~16 mantissa bits per term.  This is what lets an fp32 state survive thousands
+// of tokens within 2e-3 while running at the bf16 matrix-core rate.  The off-diagonal
+// block of T takes fp32 MFMA (16x16x4).
 //
 // Register-resident chaining.  In the 16x16x32 layout lane (q = lane/16, r = lane%16)
 // holds A[m = r][k = 8q + e], B[k = 8q + e][n = r] and D[m = 4q + i][n = r].  The
@@ -293,13 +294,29 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     return c;
   };
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
-  // Issued in the order the loop issues them (gates, keys, values), so that the wait for
+  // The same product on bf16 MFMA (16x16x16): a 16x16 block in the accumulator layout
+  // split hi/lo into two packed words each, which is exactly the operand layout of that
+  // MFMA for the left factor's transpose and for the right factor; three products
+  // l_lo r_hi + l_hi r_lo + l_hi r_hi, as for every other product here.
+  struct Split4 { uint2 h, l; };
+  auto split4 = [](const f32x4 x) {
+    Split4 s;
+    split2(x[0], x[1], s.h.x, s.l.x);
+    split2(x[2], x[3], s.h.y, s.l.y);
+    return s;
+  };
+  auto mulb = [](const Split4& lt, const Split4& rt, f32x4 c) {
+    c = mma16(lt.l, rt.h, c);
+    c = mma16(lt.h, rt.l, c);
+    return mma16(lt.h, rt.h, c);
+  };
+  // Issued in the order the loop issues them (keys, gates, values), so that the wait for
   // a chunk's gates at the top of the loop is the same count on entry as on the back edge
   // and does not also wait for the values.
   __builtin_amdgcn_sched_barrier(0);
-  fetch_g(0);
-  __builtin_amdgcn_sched_barrier(0);
   fetch_k(0);
+  __builtin_amdgcn_sched_barrier(0);
+  fetch_g(0);
   __builtin_amdgcn_sched_barrier(0);
   fetch_v(0);
   __builtin_amdgcn_sched_barrier(0);
@@ -356,7 +373,6 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       for (int i = 0; i < 4; ++i) Gl[i] += base;
     }
     if (tid < C) sBeta[tid] = braw;
-    fetch_g(t0 + C);   // the next chunk's gates (zeros past the window)
     f32x4 gam;   // 2^{G_C} on channels c4 .. c4 + 3
 #pragma unroll
     for (int j = 0; j < 4; ++j) gam[j] = ex2(gc[j]);
@@ -554,12 +570,15 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       }
     }
 
-    // ---- diagonal blocks of T = (I + A)^{-1} on fp32 MFMA, and X = K_G S' ---------------
+    // ---- diagonal blocks of T = (I + A)^{-1} on bf16 MFMA, and X = K_G S' ---------------
     // A strictly lower 16x16 block B has B^16 = 0, so (I + B)^{-1} = X1 X2 exactly with
-    // X1 = (I - B)(I + B^2) and X2 = (I + B^4)(I + B^8): eight chained 16x16x16 products
-    // (four 16x16x4 MFMAs each) in five dependent levels, each power carried together with
-    // its transpose.  Waves 0 and 2 invert their block with the steps of X in between (the
-    // two are independent, so the matrix pipe overlaps them); waves 1 and 3 only form X.
+    // X1 = (I - B)(I + B^2) and X2 = (I + B^4)(I + B^8): eight chained 16x16x16 products in
+    // five dependent levels, each power carried together with its transpose.  A product
+    // takes its factors split hi/lo on the 16x16x16 bf16 MFMA (three of them, the same three
+    // terms as every other product here), a third of the matrix-pipe time of the four fp32
+    // 16x16x4 MFMAs it replaces.  Waves 0 and 2 invert their block with the steps of X in
+    // between (the two are independent, so the matrix pipe overlaps them); waves 1 and 3
+    // only form X.
     fetch_k(t0 + C);   // the next chunk's keys
     x_init();
     if (w == 0 || w == 2) {
@@ -568,18 +587,21 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
       for (int i = 0; i < 4; ++i) id[i] = 4 * q + i == r ? 1.f : 0.f;
       const f32x4 imt = id - at;                           // (I - B)^T
-      const f32x4 p2 = mul(at, a, zero4);                  // B^2
-      const f32x4 p2t = mul(a, at, zero4);                 // (B^2)^T
+      const Split4 sa = split4(a), sat = split4(at);
+      const f32x4 p2 = mulb(sat, sa, zero4);               // B^2
+      const f32x4 p2t = mulb(sa, sat, zero4);              // (B^2)^T
       x_step(0);
-      const f32x4 p4 = mul(p2t, p2, zero4);                // B^4
-      const f32x4 p4t = mul(p2, p2t, zero4);               // (B^4)^T
-      const f32x4 x1t = mul(p2, imt, imt);                 // X1^T = (I + B^2)^T (I - B)^T
+      const Split4 s2 = split4(p2), s2t = split4(p2t);
+      const f32x4 p4 = mulb(s2t, s2, zero4);               // B^4
+      const f32x4 p4t = mulb(s2, s2t, zero4);              // (B^4)^T
+      const f32x4 x1t = mulb(s2, split4(imt), imt);        // X1^T = (I + B^2)^T (I - B)^T
       x_step(1);
-      const f32x4 p8 = mul(p4t, p4, zero4) + id;           // I + B^8
+      const Split4 s4t = split4(p4t);
+      const f32x4 p8 = mulb(s4t, split4(p4), zero4) + id;  // I + B^8
       x_step(2);
-      const f32x4 x2 = mul(p4t, p8, p8);                   // X2
+      const f32x4 x2 = mulb(s4t, split4(p8), p8);          // X2
       x_step(3);
-      const f32x4 tb = mul(x1t, x2, zero4);                // T block: rows 4q + i, column r
+      const f32x4 tb = mulb(split4(x1t), split4(x2), zero4);   // T block: rows 4q + i, column r
       const float bs = sBeta[base + r];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -594,6 +616,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) x_step(kk);
     }
+    fetch_g(t0 + C);   // the next chunk's gates (zeros past the window)
     __syncthreads();
 
     // ---- block (1, 0) of -T' = -T Diag(beta): T10 = -T11 A10 T00, formed by every wave as

@@ -118,6 +118,14 @@ __device__ inline f32x4 mma3(bf16x8 ah, bf16x8 al, bf16x8 bh, bf16x8 bl, f32x4 c
   return mma(ah, bh, c);
 }
 
+// 16x16x16 bf16 MFMA on packed words: lane (q, r) holds A[r][4q .. 4q + 3] and
+// B[4q .. 4q + 3][r], two bf16 per word
+__device__ inline f32x4 mma16(uint2 a, uint2 b, f32x4 c) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a),
+                                                   __builtin_bit_cast(s16x4, b), c, 0, 0, 0);
+}
+
 __device__ inline f32x4 mma32(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
