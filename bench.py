@@ -20,11 +20,9 @@ Order of work on the GPU:
   1. per-kernel durations of the step's kernels, from HIP events around batches of
      back-to-back launches of one kernel (median over batches);
   2. the headline: --warmup untimed steps, then exactly --steps timed steps between
-     two synchronisations.  The refresh kernel's own duration drifts with the GPU's
-     clock under sustained load (in a kernel trace of one run: ~306 us for the first
-     launches, up to ~350 us within ten steps, then down to ~270 us after a few hundred
-     launches), so a short timed region measured first thing reads ~15% slower per step
-     than the same region after step 1;
+     two synchronisations.  The refresh kernel's own duration follows the GPU's clock,
+     which drops under sudden sustained load and recovers, so the same steps measured
+     first thing (step 0) read 5-20% slower per step than here, after step 1;
   3. the other configurations, as extra keys: the full-model KDA checkpoint set (24
      layers, 256 checkpoints, T = 8 rank slices) pack/restore, and the Qwen-GDN refresh
      of 8 requests x 36 layers (`extra`);
