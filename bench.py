@@ -2,11 +2,13 @@
 """Benchmark of the DASC state-checkpoint hot path on one MI355X.
 
 One step = one pass of the whole device path over one batch of synthetic input:
-    pack     64 Kimi-Linear-shaped KDA layer states (32 heads, 128x128 fp32,
-             1556 of 4096 rows kept = 38%) into ragged checkpoints,
-    restore  the 64 checkpoints into fresh active states (omitted rows = +0.0),
-    refresh  16 of them by replaying W = 1024 suffix tokens of the gated delta
-             rule and overwriting only the omitted rows.
+    Store    pack 64 Kimi-Linear-shaped KDA layer states (32 heads, 128x128 fp32,
+             1556 of 4096 rows kept = 38%) into ragged checkpoints;
+    Load     restore the 64 checkpoints into fresh active states (omitted rows = +0.0),
+             16 of them with refresh: replay W = 1024 suffix tokens of the gated delta
+             rule and overwrite only the omitted rows.  The 16 take the fused Load with
+             refresh (restore and replay in one launch, bit-identical to the two), the
+             other 48 the plain restore; --unfused-step restores all 64, then refreshes.
 The selection plan is built once on the host before timing (the paper builds it
 offline); its host time is reported separately.
 
@@ -69,6 +71,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
                     help="headline only: skip the full-model KDA and Qwen-GDN extra keys")
+    ap.add_argument("--unfused-step", action="store_true",
+                    help="restore every checkpoint, then refresh (two launches for the refreshed "
+                         "requests) instead of the fused Load with refresh")
     ap.add_argument("--no-other-windows", action="store_true",
                     help="time the refresh at the headline window only (counter runs average "
                          "every dispatch of a kernel, so the other windows would mix in)")
@@ -268,10 +273,25 @@ def bench_headline(torch, args):
     def refresh():
         D.dasc_refresh(sh, 0, inv_row, active, req, k, v, g, beta, W)
 
+    # The Load of the step: the refreshed requests take the fused Load with refresh (restore
+    # and replay in one launch, bit-identical to restore then refresh), the other checkpoints
+    # the plain restore.  --unfused-step restores every checkpoint, then refreshes.
+    ids_rest = _i32(torch, np.arange(n_req, n_ckpt))
+
+    def restore_rest():
+        D.dasc_restore(sh, ckpt, ids_rest, inv_row, active, ids_rest, n_rows=R)
+
+    def load_refresh():
+        D.dasc_restore_refresh(sh, 0, ckpt, req, inv_row, active, req, k, v, g, beta, W, n_rows=R)
+
     def step():
         pack()
-        restore()
-        refresh()
+        if args.unfused_step:
+            restore()
+            refresh()
+        else:
+            restore_rest()
+            load_refresh()
 
     # the headline measurement as the first GPU work of the process (cold clock)
     first_ms = timed_steps(torch, step, args)
@@ -284,8 +304,8 @@ def bench_headline(torch, args):
     t["restore_req"] = batched_ms(torch, lambda: D.dasc_restore(sh, ckpt, req, inv_row, active, req,
                                                                 n_rows=R))
     t["refresh_req"] = batched_ms(torch, refresh)
-    t["restore_refresh"] = batched_ms(torch, lambda: D.dasc_restore_refresh(
-        sh, 0, ckpt, req, inv_row, active, req, k, v, g, beta, W, n_rows=R))
+    t["restore_refresh"] = batched_ms(torch, load_refresh)
+    t["restore_rest"] = batched_ms(torch, restore_rest)
 
     per_head, heads, bytes_refresh = kda_refresh_bytes(sh, plan, n_req, W)
     bytes_pack = 2 * R * dv * 4 * n_ckpt
@@ -316,8 +336,10 @@ def bench_headline(torch, args):
                     "heads": n_req * heads, **_rate(t["refresh"], bytes_refresh)},
         "restore_refresh_fused": {
             "ms": t["restore_refresh"], "unfused_ms": t["restore_req"] + t["refresh_req"],
-            "requests": n_req, "GBps": bytes_fused / t["restore_refresh"] / 1e6,
-            "bytes": bytes_fused},
+            "requests": n_req, "tokens_per_s": n_req * W / (t["restore_refresh"] / 1e3),
+            **_rate(t["restore_refresh"], bytes_fused)},
+        "restore_rest": {"checkpoints": n_ckpt - n_req,
+                         **_rate(t["restore_rest"], (R + rows) * dv * 4 * (n_ckpt - n_req))},
         "refresh_by_window": by_window,
         "timing": "HIP events around 10 batches of 10 back-to-back launches, median",
     }
@@ -333,7 +355,21 @@ def bench_headline(torch, args):
         extra["qwen_gdn"] = gdn_refresh_keys(torch, args)
         torch.cuda.empty_cache()
 
-    achieved = bytes_refresh / t["refresh"] / 1e6          # GB/s
+    # roofline of the step's dominant kernel: the fused Load with refresh (or, with
+    # --unfused-step, the refresh)
+    if args.unfused_step:
+        rk, r_ms, r_bytes = "refresh", t["refresh"], bytes_refresh
+        r_what = (f"{bytes_refresh} B = per refreshed head: k, v (bf16), g, beta (fp32), restored "
+                  "state read, omitted rows written")
+    else:
+        rk, r_ms, r_bytes = "restore_refresh", t["restore_refresh"], bytes_fused
+        r_what = (f"{bytes_fused} B = per refreshed head: k, v (bf16), g, beta (fp32); per request: "
+                  "each kept row of the checkpoint read once, every row of the layer written once")
+    achieved = r_bytes / r_ms / 1e6          # GB/s
+    step_desc = (f"pack {n_ckpt} checkpoints, restore {n_ckpt}, refresh {n_req} requests W={W}"
+                 if args.unfused_step else
+                 f"pack {n_ckpt} checkpoints, restore {n_ckpt - n_req}, Load with refresh of "
+                 f"{n_req} requests W={W} (restore + replay in one launch)")
     out = {
         "metric": METRIC,
         "value": n_req * W / (ms_step / 1e3),
@@ -344,19 +380,17 @@ def bench_headline(torch, args):
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": f"KDA layer 32h x 128x128 fp32: pack+restore {n_ckpt} checkpoints "
-                        f"(R={R} of {rows} rows kept), refresh {n_req} requests W={W}",
+            "workload": f"KDA layer 32h x 128x128 fp32 (R={R} of {rows} rows kept): {step_desc}",
             "n_checkpoints": n_ckpt, "n_requests": n_req, "W": W, "rows_kept": R,
             "inputs": "k,v bf16; g,beta fp32; state fp32",
         },
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": measured_traffic("kimi_headline/refresh"), "kernel": "refresh",
-                     "work_per_launch": f"{bytes_refresh} B = per refreshed head: k, v (bf16), g, "
-                                        "beta (fp32), restored state read, omitted rows written",
-                     "mfma_frac": flops_refresh / (t["refresh"] / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
-                     "mfma_busy": measured_util("kimi_headline/refresh", "mfma_busy"),
-                     "valu_active": measured_util("kimi_headline/refresh", "valu_active")},
+                     "traffic": measured_traffic(f"kimi_headline/{rk}"), "kernel": rk,
+                     "work_per_launch": r_what,
+                     "mfma_frac": flops_refresh / (r_ms / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+                     "mfma_busy": measured_util(f"kimi_headline/{rk}", "mfma_busy"),
+                     "valu_active": measured_util(f"kimi_headline/{rk}", "valu_active")},
         "first_pass_ms_per_step": first_ms,
         "kernels": kernels,
         "pack_restore_GBps": (bytes_pack + bytes_restore) / (t["pack"] + t["restore"]) / 1e6,
