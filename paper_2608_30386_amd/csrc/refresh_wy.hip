@@ -12,9 +12,13 @@
 // Work split: one 256-thread block per (request, head); wave w owns value columns
 // [32w, 32w + 32) of S' (128 x 32 fp32 = 16 MFMA accumulator tiles held in VGPRs for
 // the whole replay), tile nt holding the columns 32w + 2r + nt (r = lane % 16), so that
-// a lane's values for both tiles are one 32-bit word per token.  Everything that does not depend on S' (cumulative decays, K_G,
-// K_H, A, T') is built cooperatively in LDS each chunk; then each wave runs its three
-// chained contractions K_G S', T'(V - .), K_H^T U on its own columns.
+// a lane's values for both tiles are one 32-bit word per token.  Everything that does not
+// depend on S' (cumulative decays, K_G, K_H, A, T') is built cooperatively in LDS each
+// chunk; then each wave runs its three chained contractions K_G S', T'(V - .), K_H^T U on
+// its own columns.  The chunk's decays, K_G, Q and K_H are formed at the end of the
+// previous chunk, between its update products (K_G and Q go to LDS at once, K_H^T waits in
+// registers until every wave is done with the previous one), so that a chunk starts with A
+// and takes two barriers.
 //
 // Precision.  The products run on bf16 MFMA (16x16x32; 16x16x16 for the diagonal blocks
 // of T) with fp32 accumulation.  An fp32 operand x is split into x_hi = bf16(x) and
@@ -310,9 +314,103 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     c = mma16(lt.h, rt.l, c);
     return mma16(lt.h, rt.h, c);
   };
-  // Issued in the order the loop issues them (keys, gates, values), so that the wait for
-  // a chunk's gates at the top of the loop is the same count on entry as on the back edge
-  // and does not also wait for the values.
+  // Running sums of one chunk's gates (log2 units, floored) at this thread's four tokens
+  // and channels, and the chunk totals.  Lanes 8 cq .. 8 cq + 7 hold the eight token groups
+  // of a channel quad: within a lane quad, the values shifted up by one lane (zero into the
+  // first) are summed by two shift-and-add steps; the upper quad adds the lower quad's
+  // total (row shift of 4); all eight lanes form the chunk total as (lower total) + (upper
+  // total).  The selects are bitwise (all-ones / zero lane masks): a conditional expression
+  // lets the compiler move a DPP read under an exec mask, where a lane whose source lane is
+  // masked off reads a stale value.
+  auto gate_sums = [&](const f32x4 (&gr)[4], f32x4 (&Gl)[4], f32x4& gc) {
+    f32x4 run = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) run[j] += fmaxf(gr[i][j], kGateFloor) * kLog2e;
+      Gl[i] = run;
+    }
+    const uint32_t m_first = (og & 3) == 0 ? ~0u : 0u, m_upper = og >= 4 ? ~0u : 0u;
+    f32x4 x, base;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] = bsel(m_first, 0.f, quad_perm<0x90>(run[j]));   // [0,0,1,2]
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] += quad_perm<0x90>(x[j]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j] += quad_perm<0x40>(x[j]);                        // [0,0,0,1]
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float tq = quad_perm<0xFF>(x[j] + run[j]);                                 // [3,3,3,3]
+      const float below = row_shr<4>(tq), above = row_shl<4>(tq);
+      base[j] = x[j] + bsel(m_upper, below, 0.f);
+      gc[j] = bsel(m_upper, below + tq, tq + above);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) Gl[i] += base;
+  };
+
+  // K_H^T of the next chunk (rows c4 + j, tokens t4 .. t4 + 3, hi and lo), held in
+  // registers until every wave is done with this chunk's.
+  uint2 khh[4], khl[4];
+  // Everything of a chunk that does not depend on S', staged at the end of the previous
+  // chunk (its gates and keys are in registers by then): beta, 2^{G_C} and the per-wave
+  // fast-path flags into the chunk's parity copies, and the fast-path factors K_G = k 2^G
+  // and Q = k 2^{-G} into their buffers (free once every wave has formed the previous
+  // chunk's A and X).  When the chunk takes the strong-decay path instead, that path
+  // rebuilds every factor and these values are overwritten unused.
+  auto prepare = [&](int par) {
+    float* const sBeta = sBeta2 + par * C;
+    float* const sGam = sGam2 + par * D;
+    int* const sFast = sFast2 + par * 4;
+    f32x4 Gl[4], gc;
+    gate_sums(graw, Gl, gc);
+    if (tid < C) sBeta[tid] = braw;
+    f32x4 gam;   // 2^{G_C} on channels c4 .. c4 + 3
+#pragma unroll
+    for (int j = 0; j < 4; ++j) gam[j] = ex2(gc[j]);
+    if (og == 7) *reinterpret_cast<f32x4*>(sGam + c4) = gam;
+    {
+      const float gmin = fminf(fminf(gc[0], gc[1]), fminf(gc[2], gc[3]));
+      const int wave_fast = __all(gmin >= -kFastRange);
+      if (lane == 0) sFast[w] = wave_fast;
+    }
+    float kf[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      kf[i][0] = __uint_as_float(kq[i].x << 16);
+      kf[i][1] = __uint_as_float(kq[i].x & 0xFFFF0000u);
+      kf[i][2] = __uint_as_float(kq[i].y << 16);
+      kf[i][3] = __uint_as_float(kq[i].y & 0xFFFF0000u);
+    }
+    float qf[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int o = (t4 + i) * SK + c4;
+      float kg[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        kg[j] = kf[i][j] * ex2(Gl[i][j]);
+        qf[i][j] = kf[i][j] * ex2(-Gl[i][j]);
+      }
+      uint2 hi, lo;
+      split2(kg[0], kg[1], hi.x, lo.x);
+      split2(kg[2], kg[3], hi.y, lo.y);
+      *reinterpret_cast<uint2*>(sKGH + o) = hi;
+      *reinterpret_cast<uint2*>(sKGL + o) = lo;
+      split2(qf[i][0], qf[i][1], hi.x, lo.x);
+      split2(qf[i][2], qf[i][3], hi.y, lo.y);
+      *reinterpret_cast<uint2*>(sQH + o) = hi;
+      *reinterpret_cast<uint2*>(sQL + o) = lo;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {   // K_H^T = (Q 2^{G_C})^T
+      split2(qf[0][j] * gam[j], qf[1][j] * gam[j], khh[j].x, khl[j].x);
+      split2(qf[2][j] * gam[j], qf[3][j] * gam[j], khh[j].y, khl[j].y);
+    }
+  };
+
+  // Issued in the order the loop issues them (keys, gates, values), so that each wait
+  // counts only older loads.
   __builtin_amdgcn_sched_barrier(0);
   fetch_k(0);
   __builtin_amdgcn_sched_barrier(0);
@@ -320,6 +418,9 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
   __builtin_amdgcn_sched_barrier(0);
   fetch_v(0);
   __builtin_amdgcn_sched_barrier(0);
+  prepare(0);
+  fetch_k(C);
+  fetch_g(C);
 
   // Two blocks share a CU, and the instruction arbiter prefers the older block's waves: left
   // alone, the block placed first runs its chunks ~1.5x as fast as the other, which then
@@ -335,53 +436,8 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     float* const sBeta = sBeta2 + par * C;
     float* const sGam = sGam2 + par * D;
     int* const sFast = sFast2 + par * 4;
-    // ---- stage the prefetched gates (running sums) and beta ------------------------------
-    f32x4 Gl[4];   // G at tokens t4 + i, channels c4 .. c4 + 3
-    f32x4 gc;      // G at the chunk's last token
-    {
-      f32x4 run = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) run[j] += fmaxf(graw[i][j], kGateFloor) * kLog2e;
-        Gl[i] = run;
-      }
-      // Sums of the earlier token groups (lanes 8 cq .. 8 cq + 7 hold the eight groups of a
-      // channel quad), without branches: within a lane quad, the values shifted up by one lane
-      // (zero into the first) are summed by two shift-and-add steps; the upper quad adds the
-      // lower quad's total (row shift of 4).  All eight lanes form the chunk total as
-      // (lower total) + (upper total).
-      // The selects are bitwise (all-ones / zero lane masks): a conditional expression lets
-      // the compiler move a DPP read under an exec mask, where a lane whose source lane is
-      // masked off reads a stale value.
-      const uint32_t m_first = (og & 3) == 0 ? ~0u : 0u, m_upper = og >= 4 ? ~0u : 0u;
-      f32x4 x, base;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) x[j] = bsel(m_first, 0.f, quad_perm<0x90>(run[j]));   // [0,0,1,2]
-#pragma unroll
-      for (int j = 0; j < 4; ++j) x[j] += quad_perm<0x90>(x[j]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) x[j] += quad_perm<0x40>(x[j]);                        // [0,0,0,1]
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float tq = quad_perm<0xFF>(x[j] + run[j]);                                 // [3,3,3,3]
-        const float below = row_shr<4>(tq), above = row_shl<4>(tq);
-        base[j] = x[j] + bsel(m_upper, below, 0.f);
-        gc[j] = bsel(m_upper, below + tq, tq + above);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) Gl[i] += base;
-    }
-    if (tid < C) sBeta[tid] = braw;
-    f32x4 gam;   // 2^{G_C} on channels c4 .. c4 + 3
-#pragma unroll
-    for (int j = 0; j < 4; ++j) gam[j] = ex2(gc[j]);
-    if (og == 7) *reinterpret_cast<f32x4*>(sGam + c4) = gam;
-    {
-      const float gmin = fminf(fminf(gc[0], gc[1]), fminf(gc[2], gc[3]));
-      const int wave_fast = __all(gmin >= -kFastRange);
-      if (lane == 0) sFast[w] = wave_fast;
-    }
+    // this chunk's staged scalars and fast-path factors are complete, and every wave is done
+    // with the previous chunk
     __syncthreads();
     const int4 fl = *reinterpret_cast<const int4*>(sFast);
     const bool fast = fl.x && fl.y && fl.z && fl.w;
@@ -390,46 +446,13 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     // layout (a, at); wave 1 leaves block (1, 0) of A in the A buffer.
     f32x4 a = zero4, at = zero4;
     if (fast) {
-      // ---- fast path: K_G = k 2^G and Q = k 2^{-G} (rows = tokens), K_H^T = (Q 2^{G_C})^T,
-      // split hi/lo, straight from this thread's registers.  Q takes the gate buffer, which
-      // the fast path does not use.
-      float kf[4][4];
+      // ---- fast path: K_H^T from the registers (read only after the next barrier); K_G and
+      // Q are in LDS already
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        kf[i][0] = __uint_as_float(kq[i].x << 16);
-        kf[i][1] = __uint_as_float(kq[i].x & 0xFFFF0000u);
-        kf[i][2] = __uint_as_float(kq[i].y << 16);
-        kf[i][3] = __uint_as_float(kq[i].y & 0xFFFF0000u);
+      for (int j = 0; j < 4; ++j) {
+        *reinterpret_cast<uint2*>(sKHH + (c4 + j) * SV + t4) = khh[j];
+        *reinterpret_cast<uint2*>(sKHL + (c4 + j) * SV + t4) = khl[j];
       }
-      float qf[4][4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int o = (t4 + i) * SK + c4;
-        float kg[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          kg[j] = kf[i][j] * ex2(Gl[i][j]);
-          qf[i][j] = kf[i][j] * ex2(-Gl[i][j]);
-        }
-        uint2 hi, lo;
-        split2(kg[0], kg[1], hi.x, lo.x);
-        split2(kg[2], kg[3], hi.y, lo.y);
-        *reinterpret_cast<uint2*>(sKGH + o) = hi;
-        *reinterpret_cast<uint2*>(sKGL + o) = lo;
-        split2(qf[i][0], qf[i][1], hi.x, lo.x);
-        split2(qf[i][2], qf[i][3], hi.y, lo.y);
-        *reinterpret_cast<uint2*>(sQH + o) = hi;
-        *reinterpret_cast<uint2*>(sQL + o) = lo;
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {   // K_H^T row c4 + j, tokens t4 .. t4 + 3
-        uint2 hi, lo;
-        split2(qf[0][j] * gam[j], qf[1][j] * gam[j], hi.x, lo.x);
-        split2(qf[2][j] * gam[j], qf[3][j] * gam[j], hi.y, lo.y);
-        *reinterpret_cast<uint2*>(sKHH + (c4 + j) * SV + t4) = hi;
-        *reinterpret_cast<uint2*>(sKHL + (c4 + j) * SV + t4) = lo;
-      }
-      __syncthreads();
 
       // ---- A = Diag(beta) (strictly lower part of K_G Q^T): waves 0 and 2 a diagonal block
       // and, from the same operands swapped, its transpose; wave 1 block (1, 0).
@@ -466,11 +489,28 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       }
     } else {
       // ---- strong-decay path ------------------------------------------------------------
-      // the running decays and keys into LDS, row-major
+      // this chunk's gates and keys again (the registers hold the next chunk's by now), and
+      // their running decays, into LDS row-major
+      {
+        f32x4 gr[4], Gl[4], gc;
+        uint2 kc[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        *reinterpret_cast<f32x4*>(sG + (t4 + i) * SG + c4) = Gl[i];
-        *reinterpret_cast<uint2*>(sK + (t4 + i) * SK + c4) = kq[i];
+        for (int i = 0; i < 4; ++i) {
+          if (PER_CHANNEL) {
+            gr[i] = ldf4(rg, ((t4 + i) * D + c4) * 4, t0 * D * 4);
+          } else {
+            const float x = ldf(rg, (t4 + i) * 4, t0 * 4);
+            gr[i] = f32x4{x, x, x, x};
+          }
+          kc[i] = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(
+                                                rk, ((t4 + i) * D + c4) * 2, t0 * D * 2, 0));
+        }
+        gate_sums(gr, Gl, gc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          *reinterpret_cast<f32x4*>(sG + (t4 + i) * SG + c4) = Gl[i];
+          *reinterpret_cast<uint2*>(sK + (t4 + i) * SK + c4) = kc[i];
+        }
       }
       __syncthreads();
       // A = Diag(beta) (strictly lower part of R Q^T), three 16x16 tiles on bf16 MFMA
@@ -579,7 +619,6 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     // 16x16x4 MFMAs it replaces.  Waves 0 and 2 invert their block with the steps of X in
     // between (the two are independent, so the matrix pipe overlaps them); waves 1 and 3
     // only form X.
-    fetch_k(t0 + C);   // the next chunk's keys
     x_init();
     if (w == 0 || w == 2) {
       const int base = 8 * w;
@@ -616,7 +655,6 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) x_step(kk);
     }
-    fetch_g(t0 + C);   // the next chunk's gates (zeros past the window)
     __syncthreads();
 
     // ---- block (1, 0) of -T' = -T Diag(beta): T10 = -T11 A10 T00, formed by every wave as
@@ -688,8 +726,11 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) S[mt][nt] = mma3(ah, al, uh[nt], ul[nt], S[mt][nt] * gam);
     }
-    // (no barrier: the next chunk stages into the other copy of the per-chunk scalars, and
-    // writes the factor buffers read here only after its first barrier)
+    // ---- the next chunk's scalars and fast-path factors, between the update's products;
+    // then the gates and keys of the chunk after it (zeros past the window)
+    prepare(par ^ 1);
+    fetch_k(t0 + 2 * C);
+    fetch_g(t0 + 2 * C);
   }
 
 #pragma unroll
