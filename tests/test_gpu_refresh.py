@@ -230,6 +230,32 @@ def test_chunked_kernel_ragged_and_strong_decay(arch, W, g_lo):
         announce(f"chunked {arch} W={W} g_lo={g_lo} init={init} max rel err {err:.2e}")
 
 
+@pytest.mark.parametrize("strong_chunks", [(0, 2, 3), (1, 4)])
+def test_kda_fast_and_strong_chunks_interleaved(strong_chunks):
+    # Chunks of 32 tokens where some channel decays by more than 2^96 take the
+    # strong-decay path, the others the fast path, decided per chunk.  Here one channel of
+    # every head decays at every token of the chosen chunks (log-gate -12, floored at -10
+    # inside the kernel: 2^-461 over a chunk), so that the window switches paths at chosen
+    # chunk boundaries, including the first chunk and the ragged last one (W = 150).
+    L, H, Hqk, n_req, W = 1, 4, 2, 3, 150
+    sh = D.Shape("kda", L, H, Hqk, 128, 128)
+    rng = np.random.default_rng(7)
+    g_static = D.dasc_static_log_decay(rng.uniform(math.log(1e-4), 0, size=(L, H, 128)))
+    plan = D.dasc_plan(sh, g_static, "threshold", 0, 64)
+    inv = plan["inv_row"]
+    pool = (0.05 * rng.standard_normal((4, L, H, 128, 128))).astype(np.float32)
+    pool.reshape(4, -1, 128)[:, inv < 0] = 0.0
+    inp = _inputs_128("kda", n_req, H, Hqk, W, seed=11)
+    for c in strong_chunks:
+        inp["g"][:, :, 32 * c:32 * (c + 1), 5] = -12.0
+    slots = [2, 0, 3]
+    for init in ("restored", "zero"):
+        got = run_refresh(sh, pool, 0, inv, inp, W, init, slots=slots)
+        pairs = [(n, h) for n in range(n_req) for h in range(H)]
+        err = check(sh, pool, got, 0, inv, inp, pairs, init, slots=slots)
+        announce(f"strong chunks {strong_chunks} init={init} max rel err {err:.2e}")
+
+
 def test_chunked_and_column_kernels_agree():
     wl = WORKLOADS["kimi_layer"]
     lib, _ = plans(wl)
