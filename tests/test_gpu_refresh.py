@@ -256,6 +256,30 @@ def test_kda_fast_and_strong_chunks_interleaved(strong_chunks):
         announce(f"strong chunks {strong_chunks} init={init} max rel err {err:.2e}")
 
 
+@pytest.mark.parametrize("kernel", [None, "channel_wy"])
+def test_gdn_fast_and_strong_chunks_interleaved(kernel):
+    # The same switch with one gate per token (GDN heads): the chosen chunks decay at every
+    # token, on the GDN kernel and on the channel-wise kernel with its scalar-gate loads.
+    L, H, Hqk, n_req, W = 1, 4, 2, 3, 150
+    sh = D.Shape("gdn", L, H, Hqk, 128, 128)
+    rng = np.random.default_rng(8)
+    g_static = D.dasc_static_log_decay(rng.uniform(math.log(1e-4), 0, size=(L, H)))
+    g_static[0, 0] = math.log(1e-3) / 2.0
+    plan = D.dasc_plan(sh, g_static, "threshold", 0, 64)
+    inv = plan["inv_row"]
+    pool = (0.05 * rng.standard_normal((4, L, H, 128, 128))).astype(np.float32)
+    pool.reshape(4, -1, 128)[:, inv < 0] = 0.0
+    inp = _inputs_128("gdn", n_req, H, Hqk, W, seed=12)
+    for c in (0, 2, 3):
+        inp["g"][:, 1:, 32 * c:32 * (c + 1)] = -12.0
+    slots = [1, 3, 0]
+    for init in ("restored", "zero"):
+        got = run_refresh(sh, pool, 0, inv, inp, W, init, slots=slots, kernel=kernel)
+        pairs = [(n, h) for n in range(n_req) for h in range(H)]
+        err = check(sh, pool, got, 0, inv, inp, pairs, init, slots=slots)
+        announce(f"gdn strong chunks kernel={kernel} init={init} max rel err {err:.2e}")
+
+
 def test_chunked_and_column_kernels_agree():
     wl = WORKLOADS["kimi_layer"]
     lib, _ = plans(wl)
