@@ -115,6 +115,10 @@ static_assert(LDS_BYTES <= 81920, "two blocks per CU");
 
 __device__ inline float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
+// The lanes of one wave see each other's LDS writes: the wave waits for its LDS accesses
+// to finish, and the compiler moves no memory access across the wait.
+__device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 // Packed checkpoint of the fused variant (unused when FUSED is false).
 using dasc::CkptView;
 
@@ -454,14 +458,14 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         *reinterpret_cast<uint2*>(sKHL + (c4 + j) * SV + t4) = khl[j];
       }
 
-      // ---- A = Diag(beta) (strictly lower part of K_G Q^T): waves 0 and 2 a diagonal block
-      // and, from the same operands swapped, its transpose; wave 1 block (1, 0).
+      // ---- A = Diag(beta) (strictly lower part of K_G Q^T): waves 0 and 2 a diagonal block,
+      // and its transpose by a round trip through their own corner of the A buffer (the
+      // wave reads back what it wrote, so no block barrier); wave 1 block (1, 0).
       if (w < 3) {
         const int ti = w == 0 ? 0 : 1, si = w == 2 ? 1 : 0;
         const int tr = 16 * ti + r, sr = 16 * si + r;
         const f32x4 bt = *reinterpret_cast<const f32x4*>(sBeta + 16 * ti + 4 * q);
-        const float bs = sBeta[tr];
-        f32x4 acc = zero4, acc2 = zero4, tacc = zero4, tacc2 = zero4;
+        f32x4 acc = zero4, acc2 = zero4;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
           const int ot = tr * SK + 32 * kk + 4 * q, os = sr * SK + 32 * kk + 4 * q;
@@ -469,22 +473,21 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
           const bf16x8 bh = ld_op(sQH + os), bl = ld_op(sQL + os);
           if (kk & 1) acc2 = mma3(ah, al, bh, bl, acc2);
           else acc = mma3(ah, al, bh, bl, acc);
-          if (w != 1) {
-            if (kk & 1) tacc2 = mma3(bh, bl, ah, al, tacc2);
-            else tacc = mma3(bh, bl, ah, al, tacc);
-          }
         }
         acc += acc2;
-        tacc += tacc2;
         if (w == 1) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) sA[(16 + 4 * q + i) * ST + r] = bt[i] * acc[i];
         } else {
+          const int base = 8 * w;
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             a[i] = r < 4 * q + i ? bt[i] * acc[i] : 0.f;    // A[base + 4q + i][base + r]
-            at[i] = 4 * q + i < r ? bs * tacc[i] : 0.f;     // A[base + r][base + 4q + i]
+            sA[(base + 4 * q + i) * ST + base + r] = a[i];
           }
+          wave_lds_sync();
+#pragma unroll
+          for (int i = 0; i < 4; ++i) at[i] = sA[(base + r) * ST + base + 4 * q + i];   // A[base + r][base + 4q + i]
         }
       }
     } else {
