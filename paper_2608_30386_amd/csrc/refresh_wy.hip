@@ -119,6 +119,14 @@ __device__ inline float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) <<
 // to finish, and the compiler moves no memory access across the wait.
 __device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+// K_G, Q (along channels) and K_H^T (along tokens) are stored interleaved within each
+// group of 32: the four entries at 4q .. 4q + 3 and the four at 16 + 4q .. 16 + 4q + 3,
+// which one lane feeds to a contraction step in the register-chained index order, sit
+// side by side at 8q, so that the lane reads its operand in one 16-byte access.  ilv maps
+// a 4-aligned index to its stored position.
+__device__ inline int ilv(int x) { return (x & ~31) | ((x & 15) << 1) | ((x & 16) >> 2); }
+__device__ inline bf16x8 ld16(const __bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
+
 // Packed checkpoint of the fused variant (unused when FUSED is false).
 using dasc::CkptView;
 
@@ -280,8 +288,8 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     }
 #pragma unroll
     for (int mu = 0; mu < 2; ++mu) {
-      const int o = (16 * mu + r) * SK + 32 * kk + 4 * q;
-      const bf16x8 ah = ld_op(sKGH + o), al = ld_op(sKGL + o);
+      const int o = (16 * mu + r) * SK + 32 * kk + 8 * q;
+      const bf16x8 ah = ld16(sKGH + o), al = ld16(sKGL + o);
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) X[mu][nt] = mma3(ah, al, sh[nt], slo[nt], X[mu][nt]);
     }
@@ -389,7 +397,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
     float qf[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int o = (t4 + i) * SK + c4;
+      const int o = (t4 + i) * SK + ilv(c4);
       float kg[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -454,8 +462,8 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
       // Q are in LDS already
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        *reinterpret_cast<uint2*>(sKHH + (c4 + j) * SV + t4) = khh[j];
-        *reinterpret_cast<uint2*>(sKHL + (c4 + j) * SV + t4) = khl[j];
+        *reinterpret_cast<uint2*>(sKHH + (c4 + j) * SV + ilv(t4)) = khh[j];
+        *reinterpret_cast<uint2*>(sKHL + (c4 + j) * SV + ilv(t4)) = khl[j];
       }
 
       // ---- A = Diag(beta) (strictly lower part of K_G Q^T): waves 0 and 2 a diagonal block,
@@ -468,9 +476,9 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         f32x4 acc = zero4, acc2 = zero4;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-          const int ot = tr * SK + 32 * kk + 4 * q, os = sr * SK + 32 * kk + 4 * q;
-          const bf16x8 ah = ld_op(sKGH + ot), al = ld_op(sKGL + ot);
-          const bf16x8 bh = ld_op(sQH + os), bl = ld_op(sQL + os);
+          const int ot = tr * SK + 32 * kk + 8 * q, os = sr * SK + 32 * kk + 8 * q;
+          const bf16x8 ah = ld16(sKGH + ot), al = ld16(sKGL + ot);
+          const bf16x8 bh = ld16(sQH + os), bl = ld16(sQL + os);
           if (kk & 1) acc2 = mma3(ah, al, bh, bl, acc2);
           else acc = mma3(ah, al, bh, bl, acc);
         }
@@ -577,8 +585,12 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
             }
             bf16x8 hh, hl;
             split8(x, hh, hl);
-            *reinterpret_cast<bf16x8*>(sKHH + c * SV + 8 * m) = hh;
-            *reinterpret_cast<bf16x8*>(sKHL + c * SV + 8 * m) = hl;
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+              const int o = c * SV + ilv(8 * m + 4 * hf);
+              *reinterpret_cast<bf16x4*>(sKHH + o) = bf16x4{hh[4 * hf], hh[4 * hf + 1], hh[4 * hf + 2], hh[4 * hf + 3]};
+              *reinterpret_cast<bf16x4*>(sKHL + o) = bf16x4{hl[4 * hf], hl[4 * hf + 1], hl[4 * hf + 2], hl[4 * hf + 3]};
+            }
           }
         }
       }
@@ -599,8 +611,12 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         }
         bf16x8 hh, hl;
         split8(x, hh, hl);
-        *reinterpret_cast<bf16x8*>(sKGH + t * SK + c8) = hh;
-        *reinterpret_cast<bf16x8*>(sKGL + t * SK + c8) = hl;
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int o = t * SK + ilv(c8 + 4 * hf);
+          *reinterpret_cast<bf16x4*>(sKGH + o) = bf16x4{hh[4 * hf], hh[4 * hf + 1], hh[4 * hf + 2], hh[4 * hf + 3]};
+          *reinterpret_cast<bf16x4*>(sKGL + o) = bf16x4{hl[4 * hf], hl[4 * hf + 1], hl[4 * hf + 2], hl[4 * hf + 3]};
+        }
       }
       __syncthreads();
       if (w == 0 || w == 2) {
@@ -721,11 +737,8 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
     for (int mt = 0; mt < 8; ++mt) {
       const f32x4 gam = *reinterpret_cast<const f32x4*>(sGam + 16 * mt + 4 * q);
-      const int o = (16 * mt + r) * SV + 4 * q;
-      const bf16x8 ah = cat(*reinterpret_cast<const bf16x4*>(sKHH + o),
-                            *reinterpret_cast<const bf16x4*>(sKHH + o + 16));
-      const bf16x8 al = cat(*reinterpret_cast<const bf16x4*>(sKHL + o),
-                            *reinterpret_cast<const bf16x4*>(sKHL + o + 16));
+      const int o = (16 * mt + r) * SV + 8 * q;
+      const bf16x8 ah = ld16(sKHH + o), al = ld16(sKHL + o);
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) S[mt][nt] = mma3(ah, al, uh[nt], ul[nt], S[mt][nt] * gam);
     }
