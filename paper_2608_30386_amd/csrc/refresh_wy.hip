@@ -24,8 +24,7 @@
 // of T) with fp32 accumulation.  An fp32 operand x is split into x_hi = bf16(x) and
 // x_lo = bf16(x - x_hi); a product is formed as a_lo b_hi + a_hi b_lo + a_hi b_hi, which
 // keeps ~16 mantissa bits per term.  This is what lets an fp32 state survive thousands
-// of tokens within 2e-3 while running at the bf16 matrix-core rate.  The off-diagonal
-// block of T takes fp32 MFMA (16x16x4).
+// of tokens within 2e-3 while running at the bf16 matrix-core rate.
 //
 // Register-resident chaining.  In the 16x16x32 layout lane (q = lane/16, r = lane%16)
 // holds A[m = r][k = 8q + e], B[k = 8q + e][n = r] and D[m = 4q + i][n = r].  The
@@ -300,19 +299,11 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) X[mu][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
   };
-  // left * right on fp32 MFMA (16x16x4, four steps) for 16x16 blocks in the accumulator
-  // layout (lane (q, r) holds rows 4q + i of column r): the right factor as it is, the left
-  // one as its transpose (register i of lane (q, r) is then the left factor's entry at row r,
-  // contraction index 4q + i), so products chain without leaving registers.
-  auto mul = [](const f32x4 left_t, const f32x4 right, f32x4 c) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) c = mma32(left_t[i], right[i], c);
-    return c;
-  };
   const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
-  // The same product on bf16 MFMA (16x16x16): a 16x16 block in the accumulator layout
-  // split hi/lo into two packed words each, which is exactly the operand layout of that
-  // MFMA for the left factor's transpose and for the right factor; three products
+  // left * right for 16x16 blocks in the accumulator layout (lane (q, r) holds rows 4q + i
+  // of column r), on bf16 MFMA (16x16x16): each block split hi/lo into two packed words,
+  // which is exactly that MFMA's operand layout for the left factor's transpose and for
+  // the right factor, so products chain without leaving registers; three products
   // l_lo r_hi + l_hi r_lo + l_hi r_hi, as for every other product here.
   struct Split4 { uint2 h, l; };
   auto split4 = [](const f32x4 x) {
@@ -689,7 +680,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_kernel(
         t00[i] = sA[(4 * q + i) * ST + r];
       }
       const f32x4 b4 = *reinterpret_cast<const f32x4*>(sBeta + 4 * q);
-      tq = mul(t00, mul(a10, t11t, zero4), zero4) * b4;
+      tq = mulb(split4(t00), split4(mulb(split4(a10), split4(t11t), zero4)), zero4) * b4;
     }
 
     // ---- U = (-T')(X - V): the difference stays in registers as the B operand ------
