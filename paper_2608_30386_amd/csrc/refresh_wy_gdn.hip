@@ -65,6 +65,13 @@ constexpr int F_WAVE = F_B + C * 4;
 // to finish, and the compiler moves no memory access across the wait.
 __device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+// The recurrence's keys (along channels), transposed keys and values (along tokens) are
+// stored interleaved within each group of 32: the four entries at 4q .. 4q + 3 and the
+// four at 16 + 4q .. 16 + 4q + 3, which one lane feeds to a contraction step in the
+// register-chained index order, sit side by side at 8q, so that the lane reads its
+// operand in one 16-byte access.  ilv maps a 4-aligned index to its stored position.
+__device__ inline int ilv(int x) { return (x & ~31) | ((x & 15) << 1) | ((x & 16) >> 2); }
+
 // ---- recurrence kernel: LDS, two buffers by chunk parity ---------------------------------
 constexpr int SK = 136;     // bf16 [C][SK]   keys, row-major
 constexpr int SV = 40;      // bf16 [D][SV]   keys transposed; [DH][SV] values transposed
@@ -356,7 +363,9 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int u = tid + 256 * i;
-      *reinterpret_cast<uint4*>(sK + (u >> 4) * SK + (u & 15) * 8) = kraw[i];
+      const int c8 = (u & 15) * 8;
+      *reinterpret_cast<uint2*>(sK + (u >> 4) * SK + ilv(c8)) = make_uint2(kraw[i].x, kraw[i].y);
+      *reinterpret_cast<uint2*>(sK + (u >> 4) * SK + ilv(c8 + 4)) = make_uint2(kraw[i].z, kraw[i].w);
     }
     {
       uint32_t lo[4], hi[4];
@@ -366,15 +375,17 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
         hi[j] = __builtin_amdgcn_perm(kw[2 * j + 1], kw[2 * j], 0x07060302u);
       }
       const int c2 = 2 * (tid & 63), t8 = 8 * (tid >> 6);
-      *reinterpret_cast<uint4*>(sKT + c2 * SV + t8) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-      *reinterpret_cast<uint4*>(sKT + (c2 + 1) * SV + t8) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+      *reinterpret_cast<uint2*>(sKT + c2 * SV + ilv(t8)) = make_uint2(lo[0], lo[1]);
+      *reinterpret_cast<uint2*>(sKT + c2 * SV + ilv(t8 + 4)) = make_uint2(lo[2], lo[3]);
+      *reinterpret_cast<uint2*>(sKT + (c2 + 1) * SV + ilv(t8)) = make_uint2(hi[0], hi[1]);
+      *reinterpret_cast<uint2*>(sKT + (c2 + 1) * SV + ilv(t8 + 4)) = make_uint2(hi[2], hi[3]);
       const uint32_t vlo0 = __builtin_amdgcn_perm(vw[1], vw[0], 0x05040100u);
       const uint32_t vlo1 = __builtin_amdgcn_perm(vw[3], vw[2], 0x05040100u);
       const uint32_t vhi0 = __builtin_amdgcn_perm(vw[1], vw[0], 0x07060302u);
       const uint32_t vhi1 = __builtin_amdgcn_perm(vw[3], vw[2], 0x07060302u);
       const int v2 = 2 * (tid & 31), t4 = 4 * (tid >> 5);
-      *reinterpret_cast<uint2*>(sVT + v2 * SV + t4) = make_uint2(vlo0, vlo1);
-      *reinterpret_cast<uint2*>(sVT + (v2 + 1) * SV + t4) = make_uint2(vhi0, vhi1);
+      *reinterpret_cast<uint2*>(sVT + v2 * SV + ilv(t4)) = make_uint2(vlo0, vlo1);
+      *reinterpret_cast<uint2*>(sVT + (v2 + 1) * SV + ilv(t4)) = make_uint2(vhi0, vhi1);
     }
     if (w == 0) {
       const float x = chunk_log2_decay(graw, lane);
@@ -423,7 +434,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       for (int kk = 0; kk < 4; ++kk) {
 #pragma unroll
         for (int mu = 0; mu < 2; ++mu) {
-          const bf16x8 kk8 = ld_op(sK + (16 * mu + r) * SK + 32 * kk + 4 * q);
+          const bf16x8 kk8 = *reinterpret_cast<const bf16x8*>(sK + (16 * mu + r) * SK + 32 * kk + 8 * q);
           X[mu] = mma(kk8, s_lo[kk], X[mu]);
           X[mu] = mma(kk8, s_hi[kk], X[mu]);
         }
@@ -439,12 +450,14 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       f32x4 U[2];
       bf16x8 yh, yl;
       float x[8];
+      // this lane's column at tokens 4q .. 4q + 3 (mu = 0) and 16 + 4q .. (mu = 1)
+      const uint4 v4 = *reinterpret_cast<const uint4*>(sVT + (16 * w + r) * SV + 8 * q);
+      const uint32_t vw4[4] = {v4.x, v4.y, v4.z, v4.w};
 #pragma unroll
       for (int mu = 0; mu < 2; ++mu) {
-        const uint2 vv = *reinterpret_cast<const uint2*>(sVT + (16 * w + r) * SV + 16 * mu + 4 * q);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          x[4 * mu + i] = dot2(as_bf2(i < 2 ? vv.x : vv.y), (i & 1) ? kNegHi : kNegLo, X[mu][i]);
+          x[4 * mu + i] = dot2(as_bf2(vw4[2 * mu + (i >> 1)]), (i & 1) ? kNegHi : kNegLo, X[mu][i]);
       }
       split8(x, yh, yl);
 #pragma unroll
@@ -468,7 +481,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       const __bf16* sKT = reinterpret_cast<const __bf16*>(bKT(b));
 #pragma unroll
       for (int mt = 0; mt < 8; ++mt) {
-        const bf16x8 kt8 = ld_op(sKT + (16 * mt + r) * SV + 4 * q);
+        const bf16x8 kt8 = *reinterpret_cast<const bf16x8*>(sKT + (16 * mt + r) * SV + 8 * q);
         S[mt] = mma(kt8, ul, S[mt] * gam);
         S[mt] = mma(kt8, uh, S[mt]);
       }
