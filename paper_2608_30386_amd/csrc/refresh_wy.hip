@@ -93,13 +93,13 @@ constexpr int ST = 36;      // f32  [C][ST]  A, then the diagonal blocks of T
 // The A buffer keeps block (1, 0) of A; each diagonal block of A is replaced by the same
 // block of T.
 constexpr int G_BYTES = C * SG * 4 > 2 * C * SK * 2 ? C * SG * 4 : 2 * C * SK * 2;
-constexpr int OFF_G = 0;                       // f32  [C][SG]; fast path: bf16 [2][C][SK] Q
+constexpr int OFF_G = 0;                       // f32  [C][SG]; fast path: bf16 [2][C][SK] Q (ilv)
 constexpr int OFF_K = OFF_G + G_BYTES;         // bf16 [C][SK]  -> later T' diagonal blocks
 constexpr int OFF_TPH = OFF_K;                 // bf16 [C][SP]
 constexpr int OFF_TPL = OFF_TPH + C * SP * 2;
-constexpr int OFF_KGH = OFF_K + C * SK * 2;    // bf16 [C][SK]
+constexpr int OFF_KGH = OFF_K + C * SK * 2;    // bf16 [C][SK], channels interleaved (ilv)
 constexpr int OFF_KGL = OFF_KGH + C * SK * 2;
-constexpr int OFF_KHH = OFF_KGL + C * SK * 2;  // bf16 [D][SV]
+constexpr int OFF_KHH = OFF_KGL + C * SK * 2;  // bf16 [D][SV], tokens interleaved (ilv)
 constexpr int OFF_KHL = OFF_KHH + D * SV * 2;
 constexpr int OFF_A = OFF_KHL + D * SV * 2;    // f32  [C][ST]
 // Per-chunk scalars alternate between two copies by chunk parity, so that a chunk can
@@ -113,18 +113,6 @@ static_assert(2 * C * SP * 2 <= C * SK * 2, "T' must fit in the key buffer");
 static_assert(LDS_BYTES <= 81920, "two blocks per CU");
 
 __device__ inline float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
-
-// The lanes of one wave see each other's LDS writes: the wave waits for its LDS accesses
-// to finish, and the compiler moves no memory access across the wait.
-__device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-
-// K_G, Q (along channels) and K_H^T (along tokens) are stored interleaved within each
-// group of 32: the four entries at 4q .. 4q + 3 and the four at 16 + 4q .. 16 + 4q + 3,
-// which one lane feeds to a contraction step in the register-chained index order, sit
-// side by side at 8q, so that the lane reads its operand in one 16-byte access.  ilv maps
-// a 4-aligned index to its stored position.
-__device__ inline int ilv(int x) { return (x & ~31) | ((x & 15) << 1) | ((x & 16) >> 2); }
-__device__ inline bf16x8 ld16(const __bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
 // Packed checkpoint of the fused variant (unused when FUSED is false).
 using dasc::CkptView;

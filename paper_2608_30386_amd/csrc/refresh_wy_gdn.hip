@@ -61,23 +61,12 @@ constexpr int F_G = F_M + C * SA * 4;        // f32 [C]      G_t
 constexpr int F_B = F_G + C * 4;             // f32 [C]      beta_t
 constexpr int F_WAVE = F_B + C * 4;
 
-// The lanes of one wave see each other's LDS writes: the wave waits for its LDS accesses
-// to finish, and the compiler moves no memory access across the wait.
-__device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-
-// The recurrence's keys (along channels), transposed keys and values (along tokens) are
-// stored interleaved within each group of 32: the four entries at 4q .. 4q + 3 and the
-// four at 16 + 4q .. 16 + 4q + 3, which one lane feeds to a contraction step in the
-// register-chained index order, sit side by side at 8q, so that the lane reads its
-// operand in one 16-byte access.  ilv maps a 4-aligned index to its stored position.
-__device__ inline int ilv(int x) { return (x & ~31) | ((x & 15) << 1) | ((x & 16) >> 2); }
-
 // ---- recurrence kernel: LDS, two buffers by chunk parity ---------------------------------
 constexpr int SK = 136;     // bf16 [C][SK]   keys, row-major
 constexpr int SV = 40;      // bf16 [D][SV]   keys transposed; [DH][SV] values transposed
-constexpr int B_K = 0;                          // bf16 [C][SK]  keys
-constexpr int B_KT = B_K + C * SK * 2;          // bf16 [D][SV]  keys transposed
-constexpr int B_VT = B_KT + D * SV * 2;         // bf16 [DH][SV] this half's values transposed
+constexpr int B_K = 0;                          // bf16 [C][SK]  keys, channels interleaved (ilv)
+constexpr int B_KT = B_K + C * SK * 2;          // bf16 [D][SV]  keys transposed, tokens interleaved
+constexpr int B_VT = B_KT + D * SV * 2;         // bf16 [DH][SV] this half's values transposed, tokens interleaved
 constexpr int B_EG = B_VT + DH * SV * 2;        // f32  [C] 2^{G_t}
 constexpr int B_EH = B_EG + C * 4;              // f32  [C] 2^{G_C - G_t}
 constexpr int BUF = B_EH + C * 4;
@@ -434,7 +423,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       for (int kk = 0; kk < 4; ++kk) {
 #pragma unroll
         for (int mu = 0; mu < 2; ++mu) {
-          const bf16x8 kk8 = *reinterpret_cast<const bf16x8*>(sK + (16 * mu + r) * SK + 32 * kk + 8 * q);
+          const bf16x8 kk8 = ld16(sK + (16 * mu + r) * SK + 32 * kk + 8 * q);
           X[mu] = mma(kk8, s_lo[kk], X[mu]);
           X[mu] = mma(kk8, s_hi[kk], X[mu]);
         }
@@ -481,7 +470,7 @@ __global__ __launch_bounds__(256, 2) void refresh_wy_gdn_kernel(
       const __bf16* sKT = reinterpret_cast<const __bf16*>(bKT(b));
 #pragma unroll
       for (int mt = 0; mt < 8; ++mt) {
-        const bf16x8 kt8 = *reinterpret_cast<const bf16x8*>(sKT + (16 * mt + r) * SV + 8 * q);
+        const bf16x8 kt8 = ld16(sKT + (16 * mt + r) * SV + 8 * q);
         S[mt] = mma(kt8, ul, S[mt] * gam);
         S[mt] = mma(kt8, uh, S[mt]);
       }

@@ -16,6 +16,10 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 __device__ inline float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// The lanes of one wave see each other's LDS writes: the wave waits for its LDS accesses
+// to finish, and the compiler moves no memory access across the wait.
+__device__ inline void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 // Raw buffer resource over exactly `bytes` bytes: a load whose total offset (vector +
 // scalar + immediate) reaches past the end returns zero instead of touching memory.
 // Tokens past a window therefore arrive as k = v = 0, g = 0, beta = 0, which are
@@ -134,10 +138,13 @@ __device__ inline bf16x8 cat(bf16x4 a, bf16x4 b) {
   return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
 }
 
-// Row-major bf16 operand with the contraction index k(q, e) of the register-chained
-// layout (four values at p, four at p + 16).
-__device__ inline bf16x8 ld_op(const __bf16* p) {
-  return cat(*reinterpret_cast<const bf16x4*>(p), *reinterpret_cast<const bf16x4*>(p + 16));
-}
+// Operand layout of the register-chained contractions.  One contraction step feeds lane
+// (q, r) the index order k(q, e) = 4q + e (e < 4), 16 + 4q + e - 4 (e >= 4) within a group
+// of 32.  Operands staged in LDS along that index are stored interleaved: the four entries
+// at 4q .. 4q + 3 and the four at 16 + 4q .. 16 + 4q + 3 sit side by side at 8q, so that
+// the lane reads its operand in one 16-byte access.  ilv maps a 4-aligned index to its
+// stored position; ld16 reads the eight entries at a stored position.
+__device__ inline int ilv(int x) { return (x & ~31) | ((x & 15) << 1) | ((x & 16) >> 2); }
+__device__ inline bf16x8 ld16(const __bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
 }  // namespace dasc_wy
